@@ -1,0 +1,203 @@
+/*
+ * lethe.h -- C ABI of the MI355X (gfx950) Lethe hot path.
+ *
+ * Lethe (arXiv 2511.06029) prunes the KV cache of a decoding LLM along two
+ * axes: per layer, a budget derived from the layer's attention sparsity
+ * ("Spatial KV Cache Pruning via Layerwise Sparsity Estimation", Eq. 1-2), and
+ * over time, by Recency-Aware Selective Retention (RASR, Eq. 5) which keeps a
+ * recent window plus the tokens with the highest decayed attention score.
+ *
+ * This library implements one decode step (append, grouped-query attention,
+ * Eq. 5 score update) and the three calls of a prune round (layer sparsity and
+ * budgets, RASR selection, in-place compaction) as HIP kernels.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every pointer argument and every pointer inside lethe_cache is DEVICE
+ *    memory owned by the caller, except `cache` itself, which is a host
+ *    struct read during the call only.  The library allocates nothing.
+ *  - Calls enqueue work on `stream` and return without synchronising the
+ *    host.  The returned status covers host-checkable errors only; when it is
+ *    not LETHE_OK nothing was enqueued.
+ *  - Conditions found on the device are OR-ed into *cache->dev_status
+ *    (LETHE_DEV_* bits below); the affected sequence or segment is left
+ *    unmodified.  The caller reads the word at its own sync points.
+ *  - Calls keep no global mutable state: concurrent calls on different caches
+ *    and workspaces are safe.  Calls that share a cache or a workspace must be
+ *    ordered on one stream.
+ *
+ * Cache layout (ragged, one layout for K, V and scores)
+ * ----------------------------------------------------
+ *  Rows are head_dim elements of `dtype`.  Layer l owns rows
+ *  [l * rows_per_layer, (l + 1) * rows_per_layer).  The segment of
+ *  (layer l, sequence b, KV head h) starts at row
+ *      l * rows_per_layer + seq_base[b] + h * cap[b]
+ *  and holds cap[b] rows, of which the first len[l * num_seqs + b] are live
+ *  (the same count for every KV head of (l, b)).  Live rows are in token
+ *  order, oldest first.  score has the same row geometry with one fp32 per
+ *  row.  The caller guarantees seq_base[b] + num_kv_heads * cap[b] <=
+ *  rows_per_layer; kernels re-check it and flag LETHE_DEV_BAD_LAYOUT.
+ */
+#ifndef LETHE_H
+#define LETHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LETHE_OK = 0,
+  LETHE_ERR_INVALID = -1,     /* bad argument (null pointer, out-of-range value) */
+  LETHE_ERR_UNSUPPORTED = -2, /* valid but not built: head_dim, group size, batch */
+  LETHE_ERR_WORKSPACE = -3,   /* ws_bytes below lethe_workspace_bytes(...)         */
+  LETHE_ERR_HIP = -4          /* the HIP runtime rejected a launch                 */
+} lethe_status;
+
+typedef enum { LETHE_BF16 = 0, LETHE_F32 = 1 } lethe_dtype;
+
+/* Bits OR-ed into *dev_status by the kernels. */
+#define LETHE_DEV_APPEND_OVERFLOW 1 /* append with len == cap: sequence skipped      */
+#define LETHE_DEV_INFEASIBLE 2      /* protected rows exceed the global budget        */
+#define LETHE_DEV_BAD_LAYOUT 4      /* len < 0, len > cap or segment past the layer   */
+#define LETHE_DEV_HEAD_MISMATCH 8   /* compaction kept different counts across heads  */
+
+typedef struct {
+  void* k;                  /* dtype [num_layers][rows_per_layer][head_dim]            */
+  void* v;                  /* dtype [num_layers][rows_per_layer][head_dim]            */
+  float* score;             /* fp32  [num_layers][rows_per_layer]                      */
+  int32_t* len;             /* int32 [num_layers][num_seqs] live rows                  */
+  const int64_t* seq_base;  /* int64 [num_seqs] first row of sequence b in a layer     */
+  const int32_t* cap;       /* int32 [num_seqs] rows per (layer, sequence, KV head)    */
+  int64_t rows_per_layer;
+  int32_t num_layers;
+  int32_t num_seqs;         /* 1 .. 1024                                               */
+  int32_t num_q_heads;
+  int32_t num_kv_heads;     /* num_q_heads / num_kv_heads in 1 .. 8                    */
+  int32_t head_dim;         /* 64 or 128                                               */
+  lethe_dtype dtype;        /* storage of k, v and of the q / k_new / v_new inputs     */
+  int32_t* dev_status;      /* int32 [1], LETHE_DEV_* bits                             */
+} lethe_cache;
+
+/* Operations, for lethe_workspace_bytes. */
+#define LETHE_OP_DECODE 0
+#define LETHE_OP_SPARSITY 1
+#define LETHE_OP_SELECT 2
+#define LETHE_OP_COMPACT 3
+
+/*
+ * Bytes of device workspace `op` needs for this cache (0 when none).  The
+ * decode workspace must be zero-filled once before its first use; every call
+ * leaves it ready for the next one.  Other workspaces need no initialisation.
+ * Returns 0 for an invalid cache description or op.
+ */
+size_t lethe_workspace_bytes(const lethe_cache* cache, int op);
+
+/*
+ * One decode step of layer `layer` for every sequence (the decoding loop of
+ * the paper's System Overview; importance update of Eq. 5 in the RASR
+ * section, summed over the query heads of each KV group and read per token).
+ *
+ *  1. Append (when k_new != NULL): for every sequence b and KV head h, row
+ *     n = len[layer][b] of the segment receives k_new[b][h][:] and
+ *     v_new[b][h][:], and its score starts at 0; len becomes n + 1.  If
+ *     n == cap[b] the whole sequence is skipped: LETHE_DEV_APPEND_OVERFLOW is
+ *     set, its cache rows, scores and len are untouched and its out rows are
+ *     filled with quiet NaN.
+ *  2. Attention: query head i = h * G + g (G = num_q_heads / num_kv_heads)
+ *     reads KV head h (the repeat-interleave of Eq. 3, never materialised):
+ *        x_j = softmax_scale * q[b][i][:] . K[j][:],  p = softmax_j(x),
+ *        out[b][i][:] = sum_j p_j V[j][:]
+ *     over all live rows j (after the append).  A sequence with no live rows
+ *     gets out = 0.
+ *  3. Score: s_j <- gamma * s_j + sum_{g < G} p_{hG+g, j} for every live row.
+ *
+ *  q       dtype [num_seqs][num_q_heads][head_dim]
+ *  k_new   dtype [num_seqs][num_kv_heads][head_dim], or NULL (no append)
+ *  v_new   dtype [num_seqs][num_kv_heads][head_dim], NULL iff k_new is NULL
+ *  gamma   decay in (0, 1]; 1 is plain accumulated attention
+ *  softmax_scale  > 0, or <= 0 for 1/sqrt(head_dim)
+ *  out     fp32 [num_seqs][num_q_heads][head_dim]
+ *  ws      at least lethe_workspace_bytes(cache, LETHE_OP_DECODE) bytes,
+ *          zero-filled before its first use.
+ * Accumulation is fp32; results match the exact result to about 1e-5
+ * relative.  Errors: LETHE_ERR_INVALID (null pointer, layer out of range,
+ * gamma outside (0, 1] or NaN, NaN scale), LETHE_ERR_UNSUPPORTED,
+ * LETHE_ERR_WORKSPACE, LETHE_ERR_HIP.
+ */
+lethe_status lethe_decode_attn_score(const lethe_cache* cache, int32_t layer, const void* q,
+                                     const void* k_new, const void* v_new, float gamma,
+                                     float softmax_scale, float* out, void* ws, size_t ws_bytes,
+                                     hipStream_t stream);
+
+/*
+ * Layer sparsity and budgets for every sequence (start of a prune round).
+ *
+ *  Sparsity (Eq. 1 applied to Eq. 2's head-summed importance): for every
+ *  (b, l), a_j = sum_h s_{l,b,h,j} over the live rows and
+ *      S = (sqrt(n) - |a|_1 / |a|_2) / (sqrt(n) - 1), clamped to [0, 1],
+ *  with S = 0 when n <= 1 or a == 0.  Accumulated in fp64, stored as fp32.
+ *  When sparsity_in != NULL, S is taken from it instead (fp32 [num_seqs][L]).
+ *
+ *  Budgets: the paper gives layers budgets from their redundancy but no
+ *  formula; this library splits the global budget of sequence b,
+ *  global_budget[b], over its layers by density weights
+ *      w_l = 1 + floor((1 - S_l) * 2^24)   (fp32 arithmetic, S clamped, NaN -> 0)
+ *  with floors f_l = min(n_l, recent + sink) and caps n_l, proportional
+ *  integer shares and largest remainders (ties to the lower layer), capped
+ *  layers fixed and the rest re-split until no cap binds.  Then
+ *  sum_l budget = global_budget exactly and f_l <= budget <= n_l.  If
+ *  sum n_l <= global_budget every budget is n_l; if sum f_l > global_budget,
+ *  LETHE_DEV_INFEASIBLE is set and every budget is n_l.
+ *
+ *  global_budget int64 [num_seqs]; sparsity_out fp32 [num_seqs][num_layers];
+ *  budget_out int32 [num_seqs][num_layers]; recent, sink >= 0.
+ *  Needs num_layers <= 256.  ws: lethe_workspace_bytes(cache, LETHE_OP_SPARSITY)
+ *  (may be 0 bytes / NULL).
+ */
+lethe_status lethe_layer_sparsity(const lethe_cache* cache, const int64_t* global_budget,
+                                  int32_t recent, int32_t sink, const float* sparsity_in,
+                                  float* sparsity_out, int32_t* budget_out, void* ws,
+                                  size_t ws_bytes, hipStream_t stream);
+
+/*
+ * RASR retention (RASR section; sink and recent sets of Algorithm 1): for every
+ * segment (l, b, h) with n live rows and budget k = max(budget[b][l], 0):
+ *   k >= n: keep every row.  Otherwise r = min(recent, k), s = min(sink, k - r),
+ *   keep rows [0, s) and [n - r, n), and among rows [s, n - r) the first
+ *   k - r - s in the order (score descending, row ascending), where +0 and
+ *   -0 tie and NaN ranks after every number.  Exactly min(n, k) rows are kept.
+ *
+ *  budget int32 [num_seqs][num_layers]; keep uint8 [num_layers][rows_per_layer]
+ *  (same geometry as score) receives 1 (keep) or 0 (evict) for live rows;
+ *  other bytes are not written.  ws: may be NULL (0 bytes).
+ */
+lethe_status lethe_rasr_select(const lethe_cache* cache, const int32_t* budget, int32_t recent,
+                               int32_t sink, uint8_t* keep, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
+ * In-place, order-preserving compaction (pruned tokens leave the cache, as
+ * the paper's System Overview and its pruning illustration describe): in
+ * every segment the live rows with keep != 0 move, in order, to the front; K,
+ * V and score rows move together and bit-exactly; len becomes the number
+ * kept.  If the KV heads of one (l, b) keep different counts, len becomes
+ * the smallest and LETHE_DEV_HEAD_MISMATCH is set.  Rows at or after the new
+ * len are unspecified.  keep: uint8 [num_layers][rows_per_layer].
+ *  ws: lethe_workspace_bytes(cache, LETHE_OP_COMPACT) bytes.
+ */
+lethe_status lethe_kv_compact(const lethe_cache* cache, const uint8_t* keep, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+const char* lethe_status_string(lethe_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LETHE_H */

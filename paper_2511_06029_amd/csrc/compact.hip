@@ -1,0 +1,149 @@
+// In-place, order-preserving compaction of K, V and score rows, gfx950.
+//
+// One block per (layer, sequence, KV head) segment.  Rows before the first
+// evicted row stay where they are.  From there the block sweeps the source rows
+// in tiles of 64: one wavefront ballots the keep flags of the tile and writes
+// the kept rows' source indices, in order, to LDS; every thread copies its
+// share of those rows (16 bytes per lane) into an LDS stage, the block
+// synchronises, and the staged rows are stored to their destinations (a
+// running prefix count).  A destination never exceeds its source, and the
+// stores of a tile only reach rows below the tile's end, so no tile overwrites
+// a row that a later tile still has to read; within a tile, every load has
+// delivered its data to LDS before the barrier that precedes the stores.
+#include "device_common.h"
+#include "lethe_internal.h"
+
+namespace lethe {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTile = 64;
+
+template <int RB>  // row bytes of K (= of V)
+__global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
+  constexpr int TPR = RB / 16;              // threads per row
+  constexpr int RPP = kThreads / TPR;       // rows per pass
+  constexpr int PASSES = kTile / RPP;
+  static_assert(kTile % RPP == 0, "tile");
+  const int h = blockIdx.x % a.HK;
+  const int b = (blockIdx.x / a.HK) % a.B;
+  const int l = blockIdx.x / (a.HK * a.B);
+  const int tid = threadIdx.x;
+  const long long cidx = ((long long)l * a.B + b) * a.HK + h;
+  const int n = a.len[(long long)l * a.B + b];
+  const int c = a.cap[b];
+  const long long base = a.seq_base[b];
+  if (n < 0 || c < 0 || n > c || base < 0 || base + (long long)a.HK * c > a.rows_per_layer) {
+    if (tid == 0) {
+      a.counts[cidx] = -1;
+      atomicOr(a.dev_status, LETHE_DEV_BAD_LAYOUT);
+    }
+    return;
+  }
+  const long long row0 = (long long)l * a.rows_per_layer + base + (long long)h * c;
+  const uint8_t* keep = a.keep + row0;
+  char* K = reinterpret_cast<char*>(a.k) + row0 * RB;
+  char* V = reinterpret_cast<char*>(a.v) + row0 * RB;
+  float* S = a.score + row0;
+
+  // First evicted row.
+  __shared__ int s_first;
+  __shared__ int s_dst[kTile];
+  __shared__ int s_cnt;
+  __shared__ uint4 stage_k[kTile][TPR];
+  __shared__ uint4 stage_v[kTile][TPR];
+  __shared__ float stage_s[kTile];
+  if (tid == 0) s_first = n;
+  __syncthreads();
+  {
+    int f = n;
+    for (int j = tid; j < n; j += kThreads)
+      if (keep[j] == 0) {
+        f = j;
+        break;
+      }
+    if (f < n) atomicMin(&s_first, f);
+  }
+  __syncthreads();
+  const int first = s_first;
+  int pos = first;  // next destination row
+  const int lane = tid & (kWave - 1);
+  for (int j0 = first; j0 < n; j0 += kTile) {
+    if (tid < kWave) {
+      const int j = j0 + lane;
+      const bool kp = j < n && keep[j] != 0;
+      const unsigned long long mask = __ballot(kp);
+      const int before = __popcll(mask & ((1ull << lane) - 1ull));
+      const int cnt = __popcll(mask);
+      // s_dst[i] = source row of the i-th kept row of the tile.
+      if (kp) s_dst[before] = j;
+      if (lane == 0) s_cnt = cnt;
+    }
+    __syncthreads();
+    const int cnt = s_cnt;
+    const int sub = tid % TPR;
+    // Stage the kept rows of the tile in LDS.  Each load's data has arrived
+    // before it is written to LDS, and the barrier after the LDS writes
+    // precedes every global store of the tile.
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int i = p * RPP + tid / TPR;
+      if (i < cnt) {
+        const long long src = s_dst[i];
+        stage_k[i][sub] = *reinterpret_cast<const uint4*>(K + src * RB + sub * 16);
+        stage_v[i][sub] = *reinterpret_cast<const uint4*>(V + src * RB + sub * 16);
+      }
+    }
+    if (tid < cnt) stage_s[tid] = S[s_dst[tid]];
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int i = p * RPP + tid / TPR;
+      if (i < cnt) {
+        const long long dst = pos + i;
+        *reinterpret_cast<uint4*>(K + dst * RB + sub * 16) = stage_k[i][sub];
+        *reinterpret_cast<uint4*>(V + dst * RB + sub * 16) = stage_v[i][sub];
+      }
+    }
+    if (tid < cnt) S[pos + tid] = stage_s[tid];
+    pos += cnt;
+    __syncthreads();  // s_dst, s_cnt and the stage are rewritten by the next tile
+  }
+  if (tid == 0) a.counts[cidx] = pos;
+}
+
+// New length of every (layer, sequence): the kept count, equal across heads.
+__global__ void compact_len_kernel(CompactArgs a) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long long)a.L * a.B) return;
+  const int* cnt = a.counts + i * a.HK;
+  int mn = cnt[0], mx = cnt[0];
+  for (int h = 1; h < a.HK; ++h) {
+    mn = min(mn, cnt[h]);
+    mx = max(mx, cnt[h]);
+  }
+  if (mn < 0) return;  // bad layout, already flagged
+  if (mn != mx) atomicOr(a.dev_status, LETHE_DEV_HEAD_MISMATCH);
+  a.len[i] = mn;
+}
+
+}  // namespace
+
+lethe_status launch_compact(const CompactArgs& a, hipStream_t s) {
+  long long nb = (long long)a.L * a.B * a.HK;
+  if (nb > 0x7fffffffLL) return LETHE_ERR_UNSUPPORTED;
+  switch (a.row_bytes) {
+    case 128: hipLaunchKernelGGL(compact_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, s, a); break;
+    case 256: hipLaunchKernelGGL(compact_kernel<256>, dim3((unsigned)nb), dim3(kThreads), 0, s, a); break;
+    case 512: hipLaunchKernelGGL(compact_kernel<512>, dim3((unsigned)nb), dim3(kThreads), 0, s, a); break;
+    default: return LETHE_ERR_UNSUPPORTED;
+  }
+  if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
+  long long nl = (long long)a.L * a.B;
+  hipLaunchKernelGGL(compact_len_kernel, dim3((unsigned)((nl + 255) / 256)), dim3(256), 0, s, a);
+  if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
+  return LETHE_OK;
+}
+
+}  // namespace lethe

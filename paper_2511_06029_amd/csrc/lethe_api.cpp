@@ -1,0 +1,189 @@
+// Host side of the C ABI: argument validation, workspace sizing and launch
+// dispatch.  Every check here runs before any HIP call, so invalid calls
+// return without touching the device.
+#include <math.h>
+
+#include "lethe_internal.h"
+
+using namespace lethe;
+
+namespace {
+
+size_t elem_bytes(lethe_dtype dt) { return dt == LETHE_BF16 ? 2 : 4; }
+
+// Host-checkable validity of a cache description.
+lethe_status check_cache(const lethe_cache* c) {
+  if (!c) return LETHE_ERR_INVALID;
+  if (!c->k || !c->v || !c->score || !c->len || !c->seq_base || !c->cap || !c->dev_status)
+    return LETHE_ERR_INVALID;
+  if (c->num_layers < 1 || c->num_seqs < 1 || c->num_q_heads < 1 || c->num_kv_heads < 1)
+    return LETHE_ERR_INVALID;
+  if (c->rows_per_layer < 1) return LETHE_ERR_INVALID;
+  if (c->num_q_heads % c->num_kv_heads != 0) return LETHE_ERR_INVALID;
+  if (c->dtype != LETHE_BF16 && c->dtype != LETHE_F32) return LETHE_ERR_INVALID;
+  if (c->head_dim != 64 && c->head_dim != 128) return LETHE_ERR_UNSUPPORTED;
+  int G = c->num_q_heads / c->num_kv_heads;
+  if (G > 8) return LETHE_ERR_UNSUPPORTED;
+  if (c->num_seqs > kMaxSeqs) return LETHE_ERR_UNSUPPORTED;
+  if (c->num_layers > kMaxLayers) return LETHE_ERR_UNSUPPORTED;
+  // Element offsets must stay within int64 and row indices within 2^40.
+  if (c->rows_per_layer > ((int64_t)1 << 40) / c->num_layers) return LETHE_ERR_UNSUPPORTED;
+  return LETHE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lethe_status_string(lethe_status s) {
+  switch (s) {
+    case LETHE_OK: return "ok";
+    case LETHE_ERR_INVALID: return "invalid argument";
+    case LETHE_ERR_UNSUPPORTED: return "unsupported configuration";
+    case LETHE_ERR_WORKSPACE: return "workspace too small";
+    case LETHE_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+size_t lethe_workspace_bytes(const lethe_cache* c, int op) {
+  if (check_cache(c) != LETHE_OK) return 0;
+  int G = c->num_q_heads / c->num_kv_heads;
+  switch (op) {
+    case LETHE_OP_DECODE:
+      return decode_ws_layout(c->num_seqs, c->num_kv_heads, G, c->head_dim, c->rows_per_layer).total;
+    case LETHE_OP_SPARSITY:
+      return 0;
+    case LETHE_OP_SELECT:
+      return 0;
+    case LETHE_OP_COMPACT:
+      return align_up((size_t)c->num_layers * c->num_seqs * c->num_kv_heads * sizeof(int32_t), 256);
+  }
+  return 0;
+}
+
+lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const void* q,
+                                     const void* k_new, const void* v_new, float gamma,
+                                     float softmax_scale, float* out, void* ws, size_t ws_bytes,
+                                     hipStream_t stream) {
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  if (layer < 0 || layer >= c->num_layers) return LETHE_ERR_INVALID;
+  if (!q || !out || !ws) return LETHE_ERR_INVALID;
+  if ((k_new == nullptr) != (v_new == nullptr)) return LETHE_ERR_INVALID;
+  if (!(gamma > 0.0f && gamma <= 1.0f)) return LETHE_ERR_INVALID;  // also rejects NaN
+  if (isnan(softmax_scale) || isinf(softmax_scale)) return LETHE_ERR_INVALID;
+  const int G = c->num_q_heads / c->num_kv_heads;
+  const int D = c->head_dim;
+  DecodeWs w = decode_ws_layout(c->num_seqs, c->num_kv_heads, G, D, c->rows_per_layer);
+  if (ws_bytes < w.total) return LETHE_ERR_WORKSPACE;
+  float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)D);
+
+  const size_t eb = elem_bytes(c->dtype);
+  const size_t layer_off = (size_t)layer * (size_t)c->rows_per_layer * (size_t)D * eb;
+  DecodeArgs a;
+  a.k = (const char*)c->k + layer_off;
+  a.v = (const char*)c->v + layer_off;
+  a.k_w = (char*)c->k + layer_off;
+  a.v_w = (char*)c->v + layer_off;
+  a.score = c->score + (size_t)layer * (size_t)c->rows_per_layer;
+  a.len = c->len + (size_t)layer * c->num_seqs;
+  a.seq_base = c->seq_base;
+  a.cap = c->cap;
+  a.rows_per_layer = c->rows_per_layer;
+  a.B = c->num_seqs;
+  a.HK = c->num_kv_heads;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.gamma = gamma;
+  a.out = out;
+  a.plan = (int32_t*)ws;
+  a.part = (float*)((char*)ws + w.part_off);
+  a.pend = (float*)((char*)ws + w.pend_off);
+  a.dev_status = c->dev_status;
+  a.nblocks = 0;  // chosen by the launcher
+  return launch_decode(a, c->dtype, D, G, stream);
+}
+
+lethe_status lethe_layer_sparsity(const lethe_cache* c, const int64_t* global_budget,
+                                  int32_t recent, int32_t sink, const float* sparsity_in,
+                                  float* sparsity_out, int32_t* budget_out, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  if (!global_budget || !sparsity_out || !budget_out) return LETHE_ERR_INVALID;
+  if (recent < 0 || sink < 0) return LETHE_ERR_INVALID;
+  SparsityArgs a;
+  a.score = c->score;
+  a.len = c->len;
+  a.seq_base = c->seq_base;
+  a.cap = c->cap;
+  a.rows_per_layer = c->rows_per_layer;
+  a.L = c->num_layers;
+  a.B = c->num_seqs;
+  a.HK = c->num_kv_heads;
+  a.global_budget = global_budget;
+  a.recent = recent;
+  a.sink = sink;
+  a.sparsity_in = sparsity_in;
+  a.sparsity_out = sparsity_out;
+  a.budget_out = budget_out;
+  a.dev_status = c->dev_status;
+  return launch_sparsity(a, stream);
+}
+
+lethe_status lethe_rasr_select(const lethe_cache* c, const int32_t* budget, int32_t recent,
+                               int32_t sink, uint8_t* keep, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  if (!budget || !keep) return LETHE_ERR_INVALID;
+  if (recent < 0 || sink < 0) return LETHE_ERR_INVALID;
+  SelectArgs a;
+  a.score = c->score;
+  a.len = c->len;
+  a.seq_base = c->seq_base;
+  a.cap = c->cap;
+  a.rows_per_layer = c->rows_per_layer;
+  a.L = c->num_layers;
+  a.B = c->num_seqs;
+  a.HK = c->num_kv_heads;
+  a.budget = budget;
+  a.recent = recent;
+  a.sink = sink;
+  a.keep = keep;
+  a.dev_status = c->dev_status;
+  return launch_select(a, stream);
+}
+
+lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  if (!keep || !ws) return LETHE_ERR_INVALID;
+  if (ws_bytes < lethe_workspace_bytes(c, LETHE_OP_COMPACT)) return LETHE_ERR_WORKSPACE;
+  CompactArgs a;
+  a.k = c->k;
+  a.v = c->v;
+  a.score = c->score;
+  a.len = c->len;
+  a.seq_base = c->seq_base;
+  a.cap = c->cap;
+  a.rows_per_layer = c->rows_per_layer;
+  a.L = c->num_layers;
+  a.B = c->num_seqs;
+  a.HK = c->num_kv_heads;
+  a.row_bytes = c->head_dim * (int32_t)elem_bytes(c->dtype);
+  a.keep = keep;
+  a.counts = (int32_t*)ws;
+  a.dev_status = c->dev_status;
+  return launch_compact(a, stream);
+}
+
+}  // extern "C"
