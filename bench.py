@@ -1,0 +1,260 @@
+#!/usr/bin/env python3
+"""Benchmark of the Lethe hot path on one MI355X.
+
+Workload: Llama-3-8B-shaped decoding (32 layers, 32 query / 8 KV heads,
+head_dim 128, bf16 cache), batch 8, a 2048-token prompt followed by generated
+tokens; Zipf key-bias attention with per-layer exponents s ~ U[0.8, 1.6];
+global budget 40% of the logical length split across layers by sparsity;
+a prune round every 512 decode steps with a recent window of 128.
+
+One benchmark step is one prune interval: 512 decode steps over all 32 layers
+(append + fused attention and Eq. 5 score update: lethe_decode_attn_score),
+then one prune round over all layers (lethe_layer_sparsity, lethe_rasr_select,
+lethe_kv_compact).  The default run (1 warm-up step + 15 timed steps) covers
+the 8192 generated tokens of the workload; inputs are resident in HBM before
+the timed region starts.
+
+The JSON line reports KV tokens scanned per second (one token = one cached
+(layer, sequence, position) row, all KV heads) over the whole timed run, the
+per-step decode latency, the prune-round latency, the HBM roofline of the
+decode call and the CPU oracle's throughput on a bounded sample.
+"""
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=15, help="timed prune intervals")
+    ap.add_argument("--warmup", type=int, default=1, help="untimed prune intervals")
+    ap.add_argument("--interval", type=int, default=None, help="decode steps per prune interval (512)")
+    ap.add_argument("--sample-every", type=int, default=16, help="decode steps between per-call event samples")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2511_06029_amd import lethe as L
+    from workloads import CONFIGS
+    from workloads.synth import ZipfCache
+
+    cfg = CONFIGS[2]
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    Lyr, B, HQ, HK, D = cfg.num_layers, cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    interval = args.interval or cfg.prune_every
+    windows = args.warmup + args.steps
+    T0 = cfg.prompt
+    cap = T0 + interval * windows
+    gamma = cfg.gamma
+    recent, sink = cfg.recent, cfg.sink
+
+    def log(msg):
+        print("[bench] " + msg, file=sys.stderr, flush=True)
+
+    log("allocating cache: %d layers x %d seqs x %d kv heads x %d rows" % (Lyr, B, HK, cap))
+    cache = L.LetheCache(Lyr, [cap] * B, HQ, HK, D, dtype="bf16", device=dev)
+    gen = ZipfCache(2, device=dev)
+    for l in range(Lyr):
+        for b in range(B):
+            K, V = gen.segment(l, b, T0, T=T0)
+            for h in range(HK):
+                s0, _ = cache.seg_rows(b, h)
+                cache.k[l, s0:s0 + T0] = K[h]
+                cache.v[l, s0:s0 + T0] = V[h]
+    cache.len.fill_(T0)
+    P = 32
+    log("generating %d decode-step input sets" % P)
+    qp = torch.empty((P, Lyr, B, HQ, D), dtype=torch.bfloat16, device=dev)
+    kp = torch.empty((P, Lyr, B, HK, D), dtype=torch.bfloat16, device=dev)
+    vp = torch.empty((P, Lyr, B, HK, D), dtype=torch.bfloat16, device=dev)
+    for t in range(P):
+        for l in range(Lyr):
+            q, k, v = gen.step(t, l, T=np.full(B, T0))
+            qp[t, l], kp[t, l], vp[t, l] = q, k, v
+    out = torch.empty((B, HQ, D), dtype=torch.float32, device=dev)
+    ws = cache.workspace(L.OP_DECODE)
+    ws_c = cache.workspace(L.OP_COMPACT)
+    S = torch.empty((B, Lyr), dtype=torch.float32, device=dev)
+    bud = torch.empty((B, Lyr), dtype=torch.int32, device=dev)
+    keep = torch.empty((Lyr, cache.rows_per_layer), dtype=torch.uint8, device=dev)
+    gbud = torch.empty(B, dtype=torch.int64, device=dev)
+    torch.cuda.synchronize()
+
+    lib = L.load()
+    cref = ctypes.byref(cache.c_struct())
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    fn = lib.lethe_decode_attn_score
+    out_p, ws_p, wsb = ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel()
+    q_ptr = [[ctypes.c_void_p(qp[t, l].data_ptr()) for l in range(Lyr)] for t in range(P)]
+    k_ptr = [[ctypes.c_void_p(kp[t, l].data_ptr()) for l in range(Lyr)] for t in range(P)]
+    v_ptr = [[ctypes.c_void_p(vp[t, l].data_ptr()) for l in range(Lyr)] for t in range(P)]
+
+    len_snap = [torch.empty((Lyr, B), dtype=torch.int32, pin_memory=True) for _ in range(windows + 1)]
+    n_samples = args.steps * ((interval + args.sample_every - 1) // args.sample_every) * Lyr
+    call_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_samples)]
+    call_meta = []
+    win_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(windows)]
+
+    def run_window(w, timed):
+        T_start = T0 + w * interval
+        len_snap[w].copy_(cache.len, non_blocking=True)
+        win_ev[w][0].record(stream)
+        for i in range(interval):
+            t = (w * interval + i) % P
+            sample = timed and (i % args.sample_every == 0)
+            for l in range(Lyr):
+                if sample:
+                    e0, e1 = call_ev[len(call_meta)]
+                    e0.record(stream)
+                rc = fn(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, ws_p, wsb, sp)
+                if sample:
+                    e1.record(stream)
+                    call_meta.append((w, i, l))
+                if rc != 0:
+                    raise RuntimeError("lethe_decode_attn_score: %s" % L.status_string(rc))
+        win_ev[w][1].record(stream)
+        T_end = T_start + interval
+        gbud.fill_(int(math.floor(cfg.budget_frac * T_end)) * Lyr)
+        L.layer_sparsity(cache, gbud, recent, sink, None, S, bud)
+        L.rasr_select(cache, bud, recent, sink, keep)
+        L.kv_compact(cache, keep, ws_c)
+        win_ev[w][2].record(stream)
+
+    log("warm-up: %d interval(s) of %d decode steps" % (args.warmup, interval))
+    for w in range(args.warmup):
+        run_window(w, False)
+    torch.cuda.synchronize()
+    log("timed: %d interval(s)" % args.steps)
+    t0 = time.perf_counter()
+    for w in range(args.warmup, windows):
+        run_window(w, True)
+        log("interval %d enqueued" % w)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    len_snap[windows].copy_(cache.len)
+    status = int(cache.dev_status[0])
+    if status != 0:
+        raise RuntimeError("device status bits set: %d" % status)
+
+    # Work accounting from the length snapshots (lengths at the start of each
+    # interval; every decode step appends one row before attending).
+    elem = 2
+    row_bytes = HK * (2 * D * elem + 8)               # K + V + score read/write, all KV heads
+    fixed_bytes = B * HQ * D * (elem + 4) + 2 * B * HK * D * elem
+    tokens = 0
+    for w in range(args.warmup, windows):
+        n0 = len_snap[w].numpy().astype(np.int64)
+        tokens += interval * int(n0.sum()) + Lyr * B * interval * (interval + 1) // 2
+    elapsed = t1 - t0
+    decode_ms = [win_ev[w][0].elapsed_time(win_ev[w][1]) for w in range(args.warmup, windows)]
+    prune_ms = [win_ev[w][1].elapsed_time(win_ev[w][2]) for w in range(args.warmup, windows)]
+    # Per-call roofline of lethe_decode_attn_score (events on the launch stream).
+    call_ms, call_bytes = [], []
+    for (e0, e1), (w, i, l) in zip(call_ev, call_meta):
+        call_ms.append(e0.elapsed_time(e1))
+        n = len_snap[w].numpy()[l].astype(np.int64) + i + 1
+        call_bytes.append(int(n.sum()) * row_bytes + fixed_bytes)
+    avg_call_s = float(np.mean(call_ms)) / 1e3
+    avg_call_bytes = float(np.mean(call_bytes))
+    achieved = avg_call_bytes / avg_call_s / 1e9
+
+    value = tokens / elapsed
+    result = {
+        "metric": "KV tokens scanned/s (fused decode-attn+score, prune rounds included)",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Zipf key-bias caches, random queries)",
+        "config": {
+            "workload": "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128",
+            "layers": Lyr, "q_heads": HQ, "kv_heads": HK, "head_dim": D, "batch": B, "storage": "bf16",
+            "prompt": T0, "generated": interval * windows, "interval": interval, "gamma": gamma,
+        },
+        "decode_step_ms": float(np.mean(decode_ms)) / interval,
+        "prune_round_us": float(np.mean(prune_ms)) * 1e3,
+        "decode_call_us": avg_call_s * 1e6,
+        "decode_hbm_gbs": achieved,
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+            "kernel": "lethe_decode_attn_score (attn_chunks_kernel + finalize_kernel)",
+            "bytes_per_launch": avg_call_bytes, "launches_sampled": len(call_ms),
+        },
+        "final_lengths_mean": float(len_snap[windows].numpy().mean()),
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(cache, args.cpu_seconds, gamma, log)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(cache, budget_s, gamma, log):
+    """The oracle's decode step on segments of the final cache, for about
+    `budget_s` seconds of one host thread, in the same unit (a token is a
+    (layer, sequence, position) row across all KV heads)."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    log("cpu baseline: oracle decode on end-state segments (%.0f s budget)" % budget_s)
+    rng = np.random.default_rng(0)
+    lens = cache.len.cpu().numpy()
+    rows = 0
+    segs = 0
+    t_cpu = 0.0
+    l = 0
+    while t_cpu < budget_s and l < cache.L:
+        for b in range(cache.B):
+            n = int(lens[l, b])
+            for h in range(cache.HK):
+                s0, _ = cache.seg_rows(b, h)
+                K = cache.k[l, s0:s0 + n].float().cpu().numpy()
+                V = cache.v[l, s0:s0 + n].float().cpu().numpy()
+                s = cache.score[l, s0:s0 + n].double().cpu().numpy()
+                q = rng.standard_normal((cache.G, cache.D)).astype(np.float32)
+                t = time.perf_counter()
+                oracle.attend(q, K, V, s, gamma, 1 / math.sqrt(cache.D))
+                t_cpu += time.perf_counter() - t
+                rows += n
+                segs += 1
+            if t_cpu >= budget_s:
+                break
+        l += 1
+    tokens = rows / cache.HK
+    return {"value": tokens / t_cpu, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": "oracle decode attention + score update on %d (layer, seq, kv-head) segments of the "
+                      "end-state cache (%d rows, %.1f s on one host thread)" % (segs, rows, t_cpu)}
+
+
+if __name__ == "__main__":
+    main()

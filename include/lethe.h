@@ -90,9 +90,8 @@ typedef struct {
 #define LETHE_OP_COMPACT 3
 
 /*
- * Bytes of device workspace `op` needs for this cache (0 when none).  The
- * decode workspace must be zero-filled once before its first use; every call
- * leaves it ready for the next one.  Other workspaces need no initialisation.
+ * Bytes of device workspace `op` needs for this cache (0 when none).  No
+ * workspace needs initialising; its contents are scratch between calls.
  * Returns 0 for an invalid cache description or op.
  */
 size_t lethe_workspace_bytes(const lethe_cache* cache, int op);
@@ -122,8 +121,7 @@ size_t lethe_workspace_bytes(const lethe_cache* cache, int op);
  *  gamma   decay in (0, 1]; 1 is plain accumulated attention
  *  softmax_scale  > 0, or <= 0 for 1/sqrt(head_dim)
  *  out     fp32 [num_seqs][num_q_heads][head_dim]
- *  ws      at least lethe_workspace_bytes(cache, LETHE_OP_DECODE) bytes,
- *          zero-filled before its first use.
+ *  ws      at least lethe_workspace_bytes(cache, LETHE_OP_DECODE) bytes.
  * Accumulation is fp32; results match the exact result to about 1e-5
  * relative.  Errors: LETHE_ERR_INVALID (null pointer, layer out of range,
  * gamma outside (0, 1] or NaN, NaN scale), LETHE_ERR_UNSUPPORTED,

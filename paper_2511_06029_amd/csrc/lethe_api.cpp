@@ -99,11 +99,12 @@ lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const 
   a.scale_log2 = scale * 1.4426950408889634f;
   a.gamma = gamma;
   a.out = out;
-  a.plan = (int32_t*)ws;
+  a.plan = (int32_t*)((char*)ws + w.plan_off);
   a.part = (float*)((char*)ws + w.part_off);
   a.pend = (float*)((char*)ws + w.pend_off);
   a.dev_status = c->dev_status;
-  a.nblocks = 0;  // chosen by the launcher
+  a.target_tasks = 0;  // chosen by the launcher
+  a.min_chunk = 0;
   return launch_decode(a, c->dtype, D, G, stream);
 }
 

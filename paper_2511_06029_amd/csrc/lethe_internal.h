@@ -13,34 +13,34 @@ namespace lethe {
 constexpr int kMaxSeqs = 1024;
 // Largest number of layers the budget split handles.
 constexpr int kMaxLayers = 256;
-// Upper bound on decode blocks; the workspace is sized for it.
+// Upper bounds on decode blocks and on the chunk target of one launch; the
+// workspace is sized for kMaxDecodeTasks + num_seqs * num_kv_heads chunks.
 constexpr int kMaxDecodeBlocks = 4096;
+constexpr int kMaxDecodeTasks = 8192;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Decode workspace layout (bytes from ws):
-//   [0, kPlanBytes)            planner output written by the attention kernel
-//   [part_off, +part_bytes)    per-chunk partial softmax states
-//   [pend_off, +pend_bytes)    per-row scaled logits of the current step
+// Decode workspace layout (bytes from ws); nothing in it needs to be
+// initialised, every word is written before it is read within a call:
+//   plan   header (chunk rows, chunk count) + n_att[kMaxSeqs] + flag[kMaxSeqs]
+//   part   per chunk and head: m, l, o[D]
+//   pend   per row and head: scaled logit of the current step
 struct DecodeWs {
-  size_t plan_bytes, part_off, part_bytes, pend_off, pend_bytes, total;
+  size_t plan_off, part_off, pend_off, total;
 };
+
+enum PlanField { kPlanC = 0, kPlanTasks = 1, kPlanHdr = 16 };
 
 inline DecodeWs decode_ws_layout(int B, int HK, int G, int D, int64_t rows_per_layer) {
   DecodeWs w;
-  // plan: header (16 ints) + n_att[B] + nch[B] + chunk_base[B+1] + flags[B]
-  w.plan_bytes = align_up(sizeof(int32_t) * (16 + 4 * (size_t)kMaxSeqs + 1), 256);
-  size_t max_chunks = (size_t)kMaxDecodeBlocks + (size_t)B * HK;
-  w.part_off = w.plan_bytes;
-  w.part_bytes = align_up(max_chunks * (size_t)G * (D + 2) * sizeof(float), 256);
-  w.pend_off = w.part_off + w.part_bytes;
-  w.pend_bytes = align_up((size_t)rows_per_layer * G * sizeof(float), 256);
-  w.total = w.pend_off + w.pend_bytes;
+  const size_t segs = (size_t)B * HK;
+  const size_t max_chunks = (size_t)kMaxDecodeTasks + segs;
+  w.plan_off = 0;
+  w.part_off = align_up(sizeof(int32_t) * (kPlanHdr + 2 * (size_t)kMaxSeqs), 256);
+  w.pend_off = w.part_off + align_up(max_chunks * (size_t)G * (D + 2) * sizeof(float), 256);
+  w.total = w.pend_off + align_up((size_t)rows_per_layer * G * sizeof(float), 256);
   return w;
 }
-
-// Plan header fields (int32 slots).
-enum PlanField { kPlanC = 0, kPlanChunks = 1, kPlanHdr = 16 };
 
 struct DecodeArgs {
   const void* k;         // layer base, rows x D of the storage type
@@ -60,10 +60,11 @@ struct DecodeArgs {
   float gamma;
   float* out;            // [B][HQ][D]
   int32_t* plan;         // ws
-  float* part;           // ws
-  float* pend;           // ws
+  float* part;
+  float* pend;
   int32_t* dev_status;
-  int32_t nblocks;
+  int32_t target_tasks;  // attention chunks to aim for (0: one per resident block)
+  int32_t min_chunk;     // smallest chunk, rows (0: default)
 };
 
 lethe_status launch_decode(const DecodeArgs& a, lethe_dtype dt, int D, int G, hipStream_t s);

@@ -168,15 +168,23 @@ class ZipfCache:
             return max(1, -(-cfg.decode_steps // cfg.epoch))
         return 1
 
-    def directions(self, l, b):
-        """Orthonormal directions u_e, shape (H_KV, E, D) float32."""
+    def directions(self, l, b=None):
+        """Orthonormal key directions u_e of layer l: shape (H_KV, E, D) for
+        one sequence b, or (B, H_KV, E, D) for all sequences."""
         torch = self.torch
         cfg = self.cfg
         E = self._epochs()
-        z = torch.randn((cfg.num_kv_heads, cfg.head_dim, E), generator=self._gen(10, l, b),
-                        device=self.device, dtype=torch.float32)
-        qm, _ = torch.linalg.qr(z)
-        return qm.transpose(1, 2).contiguous()
+        if not hasattr(self, "_dirs"):
+            self._dirs = {}
+        if l not in self._dirs:
+            us = []
+            for bb in range(cfg.batch):
+                z = torch.randn((cfg.num_kv_heads, cfg.head_dim, E), generator=self._gen(10, l, bb),
+                                device=self.device, dtype=torch.float32)
+                qm, _ = torch.linalg.qr(z)
+                us.append(qm.transpose(1, 2).contiguous())
+            self._dirs[l] = torch.stack(us)
+        return self._dirs[l] if b is None else self._dirs[l][b]
 
     def segment(self, l, b, n, T=None):
         """Cached rows [0, n) of every KV head of (l, b): K, V of shape
@@ -198,23 +206,23 @@ class ZipfCache:
         return K.to(self.dtype), V.to(self.dtype)
 
     def step(self, t, l, T=None):
-        """q (B, H_Q, D), k_new and v_new (B, H_KV, D) for decode step t of layer l."""
+        """q (B, H_Q, D), k_new and v_new (B, H_KV, D) for decode step t of
+        layer l; T (B,) are the logical lengths before the step."""
         torch = self.torch
         cfg = self.cfg
         B, H, D, G = cfg.batch, cfg.num_kv_heads, cfg.head_dim, cfg.group
-        Ts = self.lengths() if T is None else np.full(B, T)
+        Ts = torch.as_tensor(self.lengths() if T is None else np.asarray(T), device=self.device)
         e = (t // cfg.epoch) if (cfg.zipf == "drift" and cfg.epoch > 0) else 0
         g = self._gen(20, t, l)
+        u = self.directions(l)                                   # (B, H, E, D)
+        E = u.shape[2]
         q = torch.randn((B, H * G, D), generator=g, device=self.device, dtype=torch.float32)
         k = torch.randn((B, H, D), generator=g, device=self.device, dtype=torch.float32)
         v = torch.randn((B, H, D), generator=g, device=self.device, dtype=torch.float32)
+        q += math.sqrt(D) * u[:, :, min(e, E - 1)].repeat_interleave(G, dim=1)
         s_l = float(self.exponents()[l])
-        for b in range(B):
-            u = self.directions(l, b)
-            E = u.shape[1]
-            ue = u[:, min(e, E - 1)]
-            q[b] += math.sqrt(D) * ue.repeat_interleave(G, dim=0)
-            for ee in range(E):
-                rho = torch.randint(1, int(Ts[b]) + t + 2, (H,), generator=g, device=self.device).float()
-                k[b] += (-s_l * torch.log(rho))[:, None] * u[:, ee]
+        for ee in range(E):
+            U = torch.rand((B, H), generator=g, device=self.device, dtype=torch.float64)
+            rho = 1.0 + torch.floor(U * (Ts[:, None] + t + 1).double())
+            k += (-s_l * torch.log(rho)).float()[:, :, None] * u[:, :, ee]
         return q.to(self.dtype), k.to(self.dtype), v.to(self.dtype)
