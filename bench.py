@@ -206,7 +206,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-            "kernel": "lethe_decode_attn_score (attn_chunks_kernel + finalize_kernel)",
+            "kernel": "decode_bf16_kernel<128, 4> (lethe_decode_attn_score, one launch per layer call)",
             "bytes_per_launch": avg_call_bytes, "launches_sampled": len(call_ms),
         },
         "final_lengths_mean": float(len_snap[windows].numpy().mean()),

@@ -25,6 +25,13 @@
  *  - Calls keep no global mutable state: concurrent calls on different caches
  *    and workspaces are safe.  Calls that share a cache or a workspace must be
  *    ordered on one stream.
+ *  - Each cache carries a decode state (lethe_cache::state) of
+ *    lethe_state_bytes(cache) bytes that the caller allocates and zero-fills
+ *    once, before the first call; the calls keep it consistent afterwards.  It
+ *    holds the one decode step whose score update is still pending (see
+ *    lethe_decode_attn_score).  Whoever changes len, scores or the layout of
+ *    a cache other than through these calls first calls lethe_score_flush
+ *    (or zero-fills the state again, dropping a pending step).
  *
  * Cache layout (ragged, one layout for K, V and scores)
  * ----------------------------------------------------
@@ -81,6 +88,7 @@ typedef struct {
   int32_t head_dim;         /* 64 or 128                                               */
   lethe_dtype dtype;        /* storage of k, v and of the q / k_new / v_new inputs     */
   int32_t* dev_status;      /* int32 [1], LETHE_DEV_* bits                             */
+  void* state;              /* lethe_state_bytes(cache) bytes, zero-filled before use  */
 } lethe_cache;
 
 /* Operations, for lethe_workspace_bytes. */
@@ -92,9 +100,19 @@ typedef struct {
 /*
  * Bytes of device workspace `op` needs for this cache (0 when none).  No
  * workspace needs initialising; its contents are scratch between calls.
- * Returns 0 for an invalid cache description or op.
+ * Returns 0 for an invalid cache description or op (the device pointers,
+ * cache->state included, are not looked at).
  */
 size_t lethe_workspace_bytes(const lethe_cache* cache, int op);
+
+/*
+ * Bytes of the decode state of this cache: two query sets of
+ * num_layers * num_seqs * num_q_heads * head_dim elements of dtype, 8 bytes
+ * per (layer, sequence, query head), and a few words per (layer, sequence).
+ * Independent of rows_per_layer.  Returns 0 for an invalid cache description
+ * (the device pointers, cache->state included, are not looked at).
+ */
+size_t lethe_state_bytes(const lethe_cache* cache);
 
 /*
  * One decode step of layer `layer` for every sequence (the decoding loop of
@@ -114,6 +132,15 @@ size_t lethe_workspace_bytes(const lethe_cache* cache, int op);
  *     over all live rows j (after the append).  A sequence with no live rows
  *     gets out = 0.
  *  3. Score: s_j <- gamma * s_j + sum_{g < G} p_{hG+g, j} for every live row.
+ *     This update is applied one call late.  It needs the step's final
+ *     softmax maximum and sum, known only when the whole segment has been
+ *     read, so the call keeps q, the scale and the per-head statistics in
+ *     cache->state, and the next decode call on the same layer recomputes
+ *     the step's logits from the K rows it reads anyway and applies it.  lethe_score_flush, and the
+ *     start of lethe_layer_sparsity, lethe_rasr_select and lethe_kv_compact,
+ *     apply a pending step at once.  So after a decode call `score` of that
+ *     layer lacks the call's own step until one of those runs; out and len
+ *     are final when the call's work completes.
  *
  *  q       dtype [num_seqs][num_q_heads][head_dim]
  *  k_new   dtype [num_seqs][num_kv_heads][head_dim], or NULL (no append)
@@ -122,6 +149,7 @@ size_t lethe_workspace_bytes(const lethe_cache* cache, int op);
  *  softmax_scale  > 0, or <= 0 for 1/sqrt(head_dim)
  *  out     fp32 [num_seqs][num_q_heads][head_dim]
  *  ws      at least lethe_workspace_bytes(cache, LETHE_OP_DECODE) bytes.
+ * A sequence skipped for overflow or a bad layout keeps its pending step.
  * Accumulation is fp32; results match the exact result to about 1e-5
  * relative.  Errors: LETHE_ERR_INVALID (null pointer, layer out of range,
  * gamma outside (0, 1] or NaN, NaN scale), LETHE_ERR_UNSUPPORTED,
@@ -134,6 +162,8 @@ lethe_status lethe_decode_attn_score(const lethe_cache* cache, int32_t layer, co
 
 /*
  * Layer sparsity and budgets for every sequence (start of a prune round).
+ *
+ *  Applies a pending decode step first (as lethe_score_flush).
  *
  *  Sparsity (Eq. 1 applied to Eq. 2's head-summed importance): for every
  *  (b, l), a_j = sum_h s_{l,b,h,j} over the live rows and
@@ -172,7 +202,8 @@ lethe_status lethe_layer_sparsity(const lethe_cache* cache, const int64_t* globa
  *
  *  budget int32 [num_seqs][num_layers]; keep uint8 [num_layers][rows_per_layer]
  *  (same geometry as score) receives 1 (keep) or 0 (evict) for live rows;
- *  other bytes are not written.  ws: may be NULL (0 bytes).
+ *  other bytes are not written.  ws: may be NULL (0 bytes).  Applies a
+ *  pending decode step first (as lethe_score_flush).
  */
 lethe_status lethe_rasr_select(const lethe_cache* cache, const int32_t* budget, int32_t recent,
                                int32_t sink, uint8_t* keep, void* ws, size_t ws_bytes,
@@ -186,10 +217,20 @@ lethe_status lethe_rasr_select(const lethe_cache* cache, const int32_t* budget, 
  * kept.  If the KV heads of one (l, b) keep different counts, len becomes
  * the smallest and LETHE_DEV_HEAD_MISMATCH is set.  Rows at or after the new
  * len are unspecified.  keep: uint8 [num_layers][rows_per_layer].
- *  ws: lethe_workspace_bytes(cache, LETHE_OP_COMPACT) bytes.
+ *  ws: lethe_workspace_bytes(cache, LETHE_OP_COMPACT) bytes.  Applies a
+ *  pending decode step first (as lethe_score_flush), so the scores that move
+ *  are current.
  */
 lethe_status lethe_kv_compact(const lethe_cache* cache, const uint8_t* keep, void* ws,
                               size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Apply the pending decode step of every (layer, sequence) to its scores
+ * (item 3 of lethe_decode_attn_score, Eq. 5): afterwards `score` is current
+ * and no step is pending.  Needs no workspace.  Errors: LETHE_ERR_INVALID,
+ * LETHE_ERR_UNSUPPORTED, LETHE_ERR_HIP.
+ */
+lethe_status lethe_score_flush(const lethe_cache* cache, hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char* lethe_status_string(lethe_status status);

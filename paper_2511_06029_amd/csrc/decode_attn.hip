@@ -1,31 +1,33 @@
 // Decode attention fused with the RASR importance update (Eq. 5), gfx950.
 //
-// One call handles one layer for all sequences, in two kernels.
+// One launch handles one layer for every sequence.  The live rows of each
+// (sequence, KV head) segment are cut into at most `nch` chunks of a multiple
+// of 32 rows (split-K flash decoding); block (segment, c) owns chunk c, so the
+// mapping needs no plan and no length ever travels to the host.  Blocks past
+// a segment's last chunk only take part in its completion count.
 //
-// The live rows of every (sequence, KV head) segment are cut into chunks of C
-// consecutive rows (split-K flash decoding).  C is chosen on the device from
-// the live lengths (about one chunk per resident block, at least min_chunk
-// rows), so no length ever travels to the host.  Block t of a launch owns
-// chunk t; blocks past the last chunk leave at once.
-//
-// attn_kernel, one block (4 wavefronts) per chunk, bf16 storage:
-//   each wavefront walks 32-row steps of the chunk.  QK^T runs on the matrix
-//   cores as S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (16 rows x the G query
-//   heads of the KV group padded to 16; K rows are loaded straight into the
-//   operand layout, 64 contiguous bytes per row and instruction).  Softmax is
-//   online and in base 2, one head per lane.  PV runs as O^T = V^T P^T: the
-//   step's V rows are staged in the wavefront's own LDS tile and read back
-//   transposed with ds_read_b64_tr_b16; P is split into bf16 high and low
-//   parts (two MFMAs) so the products keep fp32-level accuracy.  Every row's
-//   scaled logit goes to the pending buffer, the chunk's (m, l, o) partial to
-//   the partial buffer.  fp32 storage (head_dim 64 or 128) takes a VALU path
-//   with the same outputs.  The block owning a segment's appended row also
-//   copies k_new / v_new into the cache.
-// finalize_kernel, one block per chunk: the segment's global (M, 1/L) per
-//   head from its partials; s_j <- gamma s_j + sum_g exp2(x_gj - M_g) / L_g
-//   over the chunk's rows; one slice of the segment's output combined from
-//   the partials; block 0 publishes the new lengths and the outputs of
-//   skipped or empty sequences.
+// Per block (4 wavefronts):
+//  - bf16 storage: each wavefront walks 32-row steps.  S^T = K Q^T runs on
+//    the matrix cores (v_mfma_f32_16x16x32_bf16: 16 rows x the group's G query
+//    heads padded to 16; K rows load straight into the operand layout).  The
+//    softmax is online and in base 2, one head per lane.  O^T = V^T P^T: the
+//    step's V rows are staged in the wavefront's own LDS tile and read back
+//    transposed (ds_read_b64_tr_b16); P is split into bf16 high and low parts
+//    (two MFMAs) so the products keep fp32-level accuracy.  fp32 storage takes
+//    a VALU path with the same outputs.
+//  - Eq. 5 runs one call late: the score update of a step needs the step's
+//    final max and sum per head, known only once every chunk is done.  The
+//    call keeps its query, scale and per-head (M, 1/L); the next call on the
+//    layer recomputes that step's logits from the K rows it loads anyway (one
+//    more MFMA chain, Q_prev K^T) and applies
+//        s <- gamma s + sum_g exp2(x_g - M_g) / L_g
+//    to those rows.  launch_flush applies a pending step on its own.
+//  - The chunk's (m, l, o) partial goes to the workspace with write-through
+//    stores, then the block bumps its segment's counter.  The last block of a
+//    segment bumps the sequence's counter (the last segment of a sequence
+//    publishes its new length and pending step: every block of the sequence
+//    has read them by then) and combines the partials into out and the step's
+//    (M, 1/L) per head.  Counters go back to zero.
 #include <math.h>
 #include <stdlib.h>
 
@@ -38,9 +40,6 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kNumWaves = kThreads / kWave;
-constexpr int kFlagOverflow = 1;
-constexpr int kFlagBad = 4;
-constexpr int kFlagAppended = 16;
 constexpr float kNegBig = -1.0e30f;  // running-max start: finite, below any logit
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -50,106 +49,39 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
 typedef __attribute__((address_space(3))) char lds_char_t;
 
-// ---------------------------------------------------------------------------
-// Chunk plan (identical in every block: a pure function of len, cap, seq_base)
-// ---------------------------------------------------------------------------
-struct PlanLds {
-  int n_att[kMaxSeqs];     // rows attended (after the append); 0 when skipped
-  int base[kMaxSeqs + 1];  // first chunk of the sequence (prefix of HK * nch)
-  unsigned char flag[kMaxSeqs];
-  int C;
-  int tasks;
+// Write-through store and coherent load of two floats exchanged between the
+// blocks of one launch (relaxed, agent scope: no cache maintenance, no
+// ordering; p is 8-byte aligned).
+__device__ inline void st_agent2(float* p, float x, float y) {
+  const uint64_t v = (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline float2 ld_agent2(const float* p) {
+  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+
+// What one block works on.
+struct Chunk {
+  int b, h, seg, c;
+  int r0, r1;        // rows [r0, r1) of the segment (r1 - 1 may be the appended row)
+  int ncache;        // rows already in the cache; the appended row is row ncache
+  bool app;          // a row is appended to this sequence
+  long long segrow0; // first row of the segment in the layer
 };
 
-__device__ inline long long wave_sum_ll(long long v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
-// Chunk size and prefix of chunk counts, by wave 0, from n_att already in P.
-__device__ void plan_chunks(const DecodeArgs& a, PlanLds& P, int C_given) {
-  const int lane = threadIdx.x;
-  long long C = C_given;
-  if (C <= 0) {
-    long long total = 0;
-    for (int b0 = 0; b0 < a.B; b0 += kWave) {
-      const int b = b0 + lane;
-      total += wave_sum_ll(b < a.B ? (long long)a.HK * P.n_att[b] : 0);
-    }
-    const long long per = (total + a.target_tasks - 1) / a.target_tasks;
-    C = ((per + 63) / 64) * 64;
-    if (C < a.min_chunk) C = a.min_chunk;
-  }
-  int carry = 0;
-  for (int b0 = 0; b0 < a.B; b0 += kWave) {
-    const int b = b0 + lane;
-    const int v = (b < a.B) ? a.HK * (int)((P.n_att[b] + C - 1) / C) : 0;
-    int inc = v;
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int t = __shfl_up(inc, o);
-      if (lane >= o) inc += t;
-    }
-    if (b < a.B) P.base[b] = carry + inc - v;
-    carry += __shfl(inc, kWave - 1);
-  }
-  if (lane == 0) {
-    P.base[a.B] = carry;
-    P.C = (int)C;
-    P.tasks = carry;
-  }
-}
-
-__device__ void make_plan(const DecodeArgs& a, PlanLds& P) {
-  const int lane = threadIdx.x;
-  const bool app = a.k_new != nullptr;
-  for (int b0 = 0; b0 < a.B; b0 += kWave) {
-    const int b = b0 + lane;
-    if (b < a.B) {
-      const int n = a.len[b];
-      const int c = a.cap[b];
-      const long long base = a.seq_base[b];
-      const bool bad = n < 0 || c < 0 || n > c || base < 0 || base + (long long)a.HK * c > a.rows_per_layer;
-      const bool ovf = !bad && app && n >= c;
-      P.n_att[b] = (bad || ovf) ? 0 : n + (app ? 1 : 0);
-      P.flag[b] = (unsigned char)((bad ? kFlagBad : 0) | (ovf ? kFlagOverflow : 0) |
-                                  ((app && !bad && !ovf) ? kFlagAppended : 0));
-    }
-  }
-  plan_chunks(a, P, 0);
-}
-
-// Largest b with base[b] <= t (base is non-decreasing, base[0] = 0).
-__device__ inline int find_seq(const int* base, int B, int t) {
-  int lo = 0, hi = B;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (base[mid] <= t) lo = mid;
-    else hi = mid;
-  }
-  return lo;
-}
-
-struct TaskInfo {
-  int b, h, c, nc, r0, r1, ncache;
-  bool app;
-  long long segrow0;
+// The pending step of a segment: rows [0, rows) get
+//   s <- gamma s + sum_g exp2(scale * q_g . k - M_g) * invL_g
+// with q the step's queries (qprev half `par`) and (M, invL) from segstat.
+template <int G>
+struct Pending {
+  float* score;         // segment base
+  const float* stat;    // M[G], then invL[G]
+  const void* q;        // [G][D] storage type
+  int rows;
+  float gamma;
+  float scale;          // softmax scale * log2(e) of that step
 };
-
-__device__ inline TaskInfo task_info(const DecodeArgs& a, const PlanLds& P, int t) {
-  TaskInfo ti;
-  ti.b = find_seq(P.base, a.B, t);
-  const int na = P.n_att[ti.b];
-  ti.nc = (na + P.C - 1) / P.C;
-  const int rel = t - P.base[ti.b];
-  ti.h = rel / ti.nc;
-  ti.c = rel % ti.nc;
-  ti.r0 = ti.c * P.C;
-  ti.r1 = min(ti.r0 + P.C, na);
-  ti.app = (P.flag[ti.b] & kFlagAppended) != 0;
-  ti.ncache = na - (ti.app ? 1 : 0);
-  ti.segrow0 = a.seq_base[ti.b] + (long long)ti.h * a.cap[ti.b];
-  return ti;
-}
 
 // ---------------------------------------------------------------------------
 // Cross-wave combine of per-wave softmax states and the chunk partial.
@@ -160,26 +92,71 @@ struct CombineLds {
   float o[kNumWaves][8][128];
 };
 
+// The block's partial: per head m, l, then o[D] (pairs of floats).
 template <int D, int G>
-__device__ void write_partial(const DecodeArgs& a, const CombineLds& cb, int t) {
+__device__ void write_partial(const CombineLds& cb, float* part) {
   __syncthreads();
-  float* part = a.part + (long long)t * G * (D + 2);
-  for (int i = threadIdx.x; i < G * D; i += kThreads) {
-    const int g = i / D, d = i % D;
+  for (int i = threadIdx.x; i < G * D / 2; i += kThreads) {
+    const int g = (2 * i) / D, d = (2 * i) % D;
     float mx = kNegBig;
 #pragma unroll
     for (int k = 0; k < kNumWaves; ++k) mx = fmaxf(mx, cb.m[k][g]);
-    float lsum = 0.0f, osum = 0.0f;
+    float lsum = 0.0f, o0 = 0.0f, o1 = 0.0f;
 #pragma unroll
     for (int k = 0; k < kNumWaves; ++k) {
       const float f = exp2f(cb.m[k][g] - mx);
       lsum += cb.l[k][g] * f;
-      osum += cb.o[k][g][d] * f;
+      o0 += cb.o[k][g][d] * f;
+      o1 += cb.o[k][g][d + 1] * f;
     }
-    part[g * (D + 2) + 2 + d] = osum;
+    float* pg = part + g * (D + 2);
+    st_agent2(pg + 2 + d, o0, o1);
+    if (d == 0) st_agent2(pg, mx, lsum);
+  }
+}
+
+// Last block of a segment: out and (M, 1/L) per head from the nne partials,
+// merged in batches of up to 16 chunks with online rescaling.
+template <int D, int G>
+__device__ void combine_segment(const DecodeArgs& a, const Chunk& ck, int nne) {
+  constexpr int NB = 16;
+  const int ps = part_stride(G, D);
+  const float* part = a.part + (long long)ck.seg * a.nch * ps;
+  float* stat = a.segstat + (long long)ck.seg * 2 * G;
+  float* outb = a.out + ((long long)ck.b * a.HK * G + (long long)ck.h * G) * D;
+  for (int i = threadIdx.x; i < G * D / 2; i += kThreads) {
+    const int g = (2 * i) / D, d = (2 * i) % D;
+    const float* pg = part + g * (D + 2);
+    float M = kNegBig, lsum = 0.0f, o0 = 0.0f, o1 = 0.0f;
+    for (int c0 = 0; c0 < nne; c0 += NB) {
+      float2 ml[NB], ov[NB];
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
+        const int cc = min(c0 + k, nne - 1);
+        ml[k] = ld_agent2(pg + (long long)cc * ps);
+        ov[k] = ld_agent2(pg + (long long)cc * ps + 2 + d);
+      }
+      float bm = M;
+#pragma unroll
+      for (int k = 0; k < NB; ++k) bm = (c0 + k < nne) ? fmaxf(bm, ml[k].x) : bm;
+      const float f = exp2f(M - bm);
+      lsum *= f;
+      o0 *= f;
+      o1 *= f;
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
+        const float wgt = (c0 + k < nne) ? exp2f(ml[k].x - bm) : 0.0f;
+        lsum = fmaf(ml[k].y, wgt, lsum);
+        o0 = fmaf(ov[k].x, wgt, o0);
+        o1 = fmaf(ov[k].y, wgt, o1);
+      }
+      M = bm;
+    }
+    const float inv = 1.0f / lsum;
+    *reinterpret_cast<float2*>(outb + g * D + d) = make_float2(o0 * inv, o1 * inv);
     if (d == 0) {
-      part[g * (D + 2)] = mx;
-      part[g * (D + 2) + 1] = lsum;
+      stat[g] = M;
+      stat[G + g] = inv;
     }
   }
 }
@@ -207,13 +184,45 @@ __device__ inline bf16x8_t zero_bf16x8() {
   return z;
 }
 
+// Queries of the current and of the pending step, 16 rows each (heads past G
+// are zero), and the pending step's M and 1/L per head (zero past G), staged
+// in LDS once per block and read per step, so they take no registers across
+// the loop.  Rows are padded by 16 bytes: the 16 lanes of a group read 16
+// different rows without bank conflicts.
+template <int D>
+struct QLds {
+  static constexpr int STRIDE = 2 * D + 16;
+  char q[2][16 * STRIDE];
+  float pm[16];
+  float pi[16];
+};
+
+// Fills one query tile from [G][D] bf16 in global memory.
 template <int D, int G>
-__device__ void attn_chunk_mfma(const DecodeArgs& a, const PlanLds& P, char* vtiles, CombineLds& cb, int t) {
+__device__ inline void stage_q(char* tile, const void* src) {
+  constexpr int CPR = 2 * D / 16;  // 16-byte pieces per row
+  for (int i = threadIdx.x; i < 16 * CPR; i += kThreads) {
+    const int r = i / CPR, p = i % CPR;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (r < G) v = reinterpret_cast<const uint4*>(src)[r * CPR + p];
+    *reinterpret_cast<uint4*>(tile + r * QLds<D>::STRIDE + 16 * p) = v;
+  }
+}
+
+// MFMA operand of a staged query tile: lane holds Q[head s][32 kk + 8 g4 .. +8];
+// it serves as B of S^T = K Q^T and as A of S = Q K^T.
+template <int D>
+__device__ inline bf16x8_t q_operand(const char* tile, int s, int g4, int kk) {
+  return *reinterpret_cast<const bf16x8_t*>(tile + s * QLds<D>::STRIDE + 64 * kk + 16 * g4);
+}
+
+template <int D, int G>
+__device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pending<G>& pd, char* vtiles,
+                                QLds<D>& qs, CombineLds& cb) {
   using Cfg = MfmaCfg<D>;
   constexpr int KK = Cfg::KK, NT = Cfg::NT, ROWB = Cfg::ROWB, VSTRIDE = Cfg::VSTRIDE;
   constexpr int STEP = Cfg::STEP, LPR = Cfg::LPR, RPL = Cfg::RPL, VLOADS = Cfg::VLOADS;
-  static_assert(G <= 16, "heads of a group are padded to 16 MFMA columns");
-  const TaskInfo ti = task_info(a, P, t);
+  static_assert(G <= 8, "pending heads live in lane groups 0 and 1");
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int w = tid / kWave;
@@ -222,26 +231,28 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const PlanLds& P, char* vti
   const int HQ = a.HK * G;
   char* vb = vtiles + w * Cfg::TILE_BYTES;
 
-  // Q^T operand: lane holds Q[head s][32 kk + 8 g4 .. +8].
-  bf16x8_t qb[KK];
-  {
-    const char* qrow = reinterpret_cast<const char*>(a.q) + (((long long)ti.b * HQ + (long long)ti.h * G + s) * D) * 2;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-      qb[kk] = (s < G) ? *reinterpret_cast<const bf16x8_t*>(qrow + 64 * kk + 16 * g4) : zero_bf16x8();
+  const int re = min(ck.r1, ck.ncache);
+  const int pre_end = min(pd.rows, re);
+  stage_q<D, G>(qs.q[0], reinterpret_cast<const char*>(a.q) + ((long long)ck.b * HQ + (long long)ck.h * G) * D * 2);
+  if (pre_end > ck.r0) {
+    stage_q<D, G>(qs.q[1], pd.q);
+    if (tid < 16) {
+      qs.pm[tid] = tid < G ? pd.stat[tid] : 0.0f;
+      qs.pi[tid] = tid < G ? pd.stat[G + tid] : 0.0f;
+    }
   }
+  __syncthreads();
+
   float m = kNegBig, l = 0.0f;
   f32x4_t o[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-  const char* Kb = reinterpret_cast<const char*>(a.k) + ti.segrow0 * ROWB;
-  const char* Vb = reinterpret_cast<const char*>(a.v) + ti.segrow0 * ROWB;
-  float* pend = a.pend + ti.segrow0 * G;
+  const char* Kb = reinterpret_cast<const char*>(a.k) + ck.segrow0 * ROWB;
+  const char* Vb = reinterpret_cast<const char*>(a.v) + ck.segrow0 * ROWB;
   const float sc = a.scale_log2;
-  const int re = min(ti.r1, ti.ncache);
 
-  for (int base = ti.r0 + STEP * w; base < re; base += STEP * kNumWaves) {
+  for (int base = ck.r0 + STEP * w; base < re; base += STEP * kNumWaves) {
     bf16x8_t kr[2][KK];
 #pragma unroll
     for (int T = 0; T < 2; ++T) {
@@ -256,16 +267,44 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const PlanLds& P, char* vti
       const int row = min(base + RPL * u + lane / LPR, re - 1);
       vr[u] = *reinterpret_cast<const uint4*>(Vb + (long long)row * ROWB + 16 * (lane % LPR));
     }
+    // Pending update of this step's rows: lane groups 0 and 1 own rows
+    // base + 16 g4 + s.
+    const bool pstep = base < pre_end;
+    const int prow = base + 16 * g4 + s;
+    const bool pon = pstep && g4 < 2 && prow < pre_end;
+    float sold = 0.0f;
+    if (pon) sold = pd.score[prow];
+
     f32x4_t sacc[2];
 #pragma unroll
     for (int T = 0; T < 2; ++T) {
       sacc[T] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) sacc[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], qb[kk], sacc[T], 0, 0, 0);
+      for (int kk = 0; kk < KK; ++kk)
+        sacc[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], q_operand<D>(qs.q[0], s, g4, kk), sacc[T], 0, 0, 0);
     }
 #pragma unroll
     for (int u = 0; u < VLOADS; ++u)
       *reinterpret_cast<uint4*>(vb + (RPL * u + lane / LPR) * VSTRIDE + 16 * (lane % LPR)) = vr[u];
+    if (pstep) {
+      // S = Q_prev K^T: lane (g4, s) gets heads 4 g4 + rr of row 16 T + s.
+      const float4 pm = *reinterpret_cast<const float4*>(qs.pm + 4 * g4);
+      const float4 pi = *reinterpret_cast<const float4*>(qs.pi + 4 * g4);
+      float part[2];
+#pragma unroll
+      for (int T = 0; T < 2; ++T) {
+        f32x4_t so = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+          so = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q_operand<D>(qs.q[1], s, g4, kk), kr[T][kk], so, 0, 0, 0);
+        float acc = exp2f(fmaf(so[0], pd.scale, -pm.x)) * pi.x;
+        acc = fmaf(exp2f(fmaf(so[1], pd.scale, -pm.y)), pi.y, acc);
+        acc = fmaf(exp2f(fmaf(so[2], pd.scale, -pm.z)), pi.z, acc);
+        acc = fmaf(exp2f(fmaf(so[3], pd.scale, -pm.w)), pi.w, acc);
+        part[T] = acc + __shfl_xor(acc, 16);
+      }
+      if (pon) pd.score[prow] = fmaf(pd.gamma, sold, g4 == 0 ? part[0] : part[1]);
+    }
 
     // Logits of rows base + 16 T + 4 g4 + rr for head s.
     float x[2][4];
@@ -275,10 +314,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const PlanLds& P, char* vti
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int row = base + 16 * T + 4 * g4 + rr;
-        const float v = sacc[T][rr] * sc;
-        const bool ok = row < re;
-        if (ok && s < G) pend[(long long)row * G + s] = v;
-        x[T][rr] = ok ? v : -INFINITY;
+        x[T][rr] = row < re ? sacc[T][rr] * sc : -INFINITY;
         mx = fmaxf(mx, x[T][rr]);
       }
     }
@@ -317,22 +353,24 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const PlanLds& P, char* vti
   }
 
   // The appended row (last chunk of its segment), by wave 0: read from
-  // k_new / v_new, copied into the cache, and folded into wave 0's state.
-  if (ti.app && ti.r1 == ti.ncache + 1 && w == 0) {
-    const char* kn = reinterpret_cast<const char*>(a.k_new) + (((long long)ti.b * a.HK + ti.h) * D) * 2;
-    const char* vn = reinterpret_cast<const char*>(a.v_new) + (((long long)ti.b * a.HK + ti.h) * D) * 2;
+  // k_new / v_new, copied into the cache, its score started at 0, and folded
+  // into wave 0's state.
+  if (ck.app && ck.r1 == ck.ncache + 1 && w == 0) {
+    const char* kn = reinterpret_cast<const char*>(a.k_new) + (((long long)ck.b * a.HK + ck.h) * D) * 2;
+    const char* vn = reinterpret_cast<const char*>(a.v_new) + (((long long)ck.b * a.HK + ck.h) * D) * 2;
     if (lane < LPR) {
-      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.k_w) + (ti.segrow0 + ti.ncache) * ROWB + 16 * lane) =
+      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.k_w) + (ck.segrow0 + ck.ncache) * ROWB + 16 * lane) =
           *reinterpret_cast<const uint4*>(kn + 16 * lane);
-      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.v_w) + (ti.segrow0 + ti.ncache) * ROWB + 16 * lane) =
+      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.v_w) + (ck.segrow0 + ck.ncache) * ROWB + 16 * lane) =
           *reinterpret_cast<const uint4*>(vn + 16 * lane);
     }
+    if (lane == 0) pd.score[ck.ncache] = 0.0f;
     // x_s = scale q_s . k_new: each lane group sums its quarter of the dims.
     float acc = 0.0f;
     const uint32_t* kq = reinterpret_cast<const uint32_t*>(kn);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const bf16x8_t qv = qb[kk];
+      const bf16x8_t qv = q_operand<D>(qs.q[0], s, g4, kk);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bf16x2_t q2 = {qv[2 * j], qv[2 * j + 1]};
@@ -343,7 +381,6 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const PlanLds& P, char* vti
     acc += __shfl_xor(acc, 16);
     acc += __shfl_xor(acc, 32);
     const float x = acc * sc;
-    if (g4 == 0 && s < G) pend[(long long)ti.ncache * G + s] = x;
     const float mnew = fmaxf(m, x);
     const float corr = exp2f(m - mnew);
     const float p = exp2f(x - mnew);
@@ -374,22 +411,19 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const PlanLds& P, char* vti
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) cb.o[w][s][16 * nt + 4 * g4 + rr] = o[nt][rr];
   }
-  write_partial<D, G>(a, cb, t);
 }
 
 // ---------------------------------------------------------------------------
 // fp32 path (VALU): 16-byte loads, D/4 lanes per row.
 // ---------------------------------------------------------------------------
 template <int D, int G>
-__device__ void attn_chunk_f32(const DecodeArgs& a, const PlanLds& P, CombineLds& cb, int t) {
+__device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pending<G>& pd, CombineLds& cb) {
   constexpr int EPL = 4;
   constexpr int LPR = D / EPL;
   constexpr int RPW = kWave / LPR;
   constexpr int U = 4;
   constexpr int ROWS_WAVE = U * RPW;
   constexpr int ROWS_BLOCK = ROWS_WAVE * kNumWaves;
-  static_assert(G <= LPR, "one logit-writer lane per head");
-  const TaskInfo ti = task_info(a, P, t);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int w = tid / kWave;
@@ -397,9 +431,11 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const PlanLds& P, CombineLds
   const int dp = lane % LPR;
   const int HQ = a.HK * G;
 
-  float qf[G][EPL];
+  // Queries pre-scaled by their step's scale, so both logit sums below are
+  // formed the same way.
+  float qf[G][EPL], qof[G][EPL];
   {
-    const float* qb = reinterpret_cast<const float*>(a.q) + ((long long)ti.b * HQ + (long long)ti.h * G) * D + dp * EPL;
+    const float* qb = reinterpret_cast<const float*>(a.q) + ((long long)ck.b * HQ + (long long)ck.h * G) * D + dp * EPL;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const uint4 r = *reinterpret_cast<const uint4*>(qb + (long long)g * D);
@@ -407,6 +443,29 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const PlanLds& P, CombineLds
       qf[g][1] = __uint_as_float(r.y) * a.scale_log2;
       qf[g][2] = __uint_as_float(r.z) * a.scale_log2;
       qf[g][3] = __uint_as_float(r.w) * a.scale_log2;
+    }
+  }
+  const int re = min(ck.r1, ck.ncache);
+  const int pre_end = min(pd.rows, re);
+  float pM[G], pI[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    pM[g] = 0.0f;
+    pI[g] = 0.0f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) qof[g][e] = 0.0f;
+  }
+  if (pre_end > ck.r0) {
+    const float* qp = reinterpret_cast<const float*>(pd.q) + dp * EPL;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const uint4 r = *reinterpret_cast<const uint4*>(qp + (long long)g * D);
+      qof[g][0] = __uint_as_float(r.x) * pd.scale;
+      qof[g][1] = __uint_as_float(r.y) * pd.scale;
+      qof[g][2] = __uint_as_float(r.z) * pd.scale;
+      qof[g][3] = __uint_as_float(r.w) * pd.scale;
+      pM[g] = pd.stat[g];
+      pI[g] = pd.stat[G + g];
     }
   }
   float m[G], l[G], o[G][EPL];
@@ -417,11 +476,11 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const PlanLds& P, CombineLds
 #pragma unroll
     for (int e = 0; e < EPL; ++e) o[g][e] = 0.0f;
   }
-  const float* Kb = reinterpret_cast<const float*>(a.k) + ti.segrow0 * D + dp * EPL;
-  const float* Vb = reinterpret_cast<const float*>(a.v) + ti.segrow0 * D + dp * EPL;
-  float* pend = a.pend + ti.segrow0 * G;
+  const float* Kb = reinterpret_cast<const float*>(a.k) + ck.segrow0 * D + dp * EPL;
+  const float* Vb = reinterpret_cast<const float*>(a.v) + ck.segrow0 * D + dp * EPL;
 
-  auto consume = [&](const uint4* kr, const uint4* vr, const int* row, const bool* valid) {
+  auto consume = [&](const uint4* kr, const uint4* vr, const bool* valid, bool pstep, const int* row,
+                     const float* sold) {
     float x[U][G];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -432,17 +491,21 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const PlanLds& P, CombineLds
         float acc = 0.0f;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) acc = fmaf(qf[g][e], kf[e], acc);
-        x[u][g] = group_sum<LPR>(acc);
+        const float xs = group_sum<LPR>(acc);  // every lane takes part
+        x[u][g] = valid[u] ? xs : -INFINITY;
       }
-    }
+      if (pstep) {
+        float c = 0.0f;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float mine = x[u][0];
+        for (int g = 0; g < G; ++g) {
+          float acc = 0.0f;
 #pragma unroll
-      for (int g = 1; g < G; ++g) mine = (dp == g) ? x[u][g] : mine;
-      if (valid[u] && dp < G) pend[(long long)row[u] * G + dp] = mine;
-#pragma unroll
-      for (int g = 0; g < G; ++g) x[u][g] = valid[u] ? x[u][g] : -INFINITY;
+          for (int e = 0; e < EPL; ++e) acc = fmaf(qof[g][e], kf[e], acc);
+          const float xs = group_sum<LPR>(acc);
+          c = fmaf(exp2f(xs - pM[g]), pI[g], c);
+        }
+        if (dp == 0 && row[u] < pre_end) pd.score[row[u]] = fmaf(pd.gamma, sold[u], c);
+      }
     }
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -467,11 +530,12 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const PlanLds& P, CombineLds
     }
   };
 
-  const int re = min(ti.r1, ti.ncache);
-  for (int base = ti.r0 + w * ROWS_WAVE; base < re; base += ROWS_BLOCK) {
+  for (int base = ck.r0 + w * ROWS_WAVE; base < re; base += ROWS_BLOCK) {
     uint4 kr[U], vr[U];
     int row[U];
     bool valid[U];
+    float sold[U];
+    const bool pstep = base < pre_end;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       row[u] = base + u * RPW + rg;
@@ -479,26 +543,30 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const PlanLds& P, CombineLds
       const int rr = valid[u] ? row[u] : (re - 1);
       kr[u] = *reinterpret_cast<const uint4*>(Kb + (long long)rr * D);
       vr[u] = *reinterpret_cast<const uint4*>(Vb + (long long)rr * D);
+      sold[u] = (pstep && dp == 0 && row[u] < pre_end) ? pd.score[row[u]] : 0.0f;
     }
-    consume(kr, vr, row, valid);
+    consume(kr, vr, valid, pstep, row, sold);
   }
-  if (ti.app && ti.r1 == ti.ncache + 1 && w == 0) {
-    const long long nb = ((long long)ti.b * a.HK + ti.h) * D + dp * EPL;
+  if (ck.app && ck.r1 == ck.ncache + 1 && w == 0) {
+    const long long nb = ((long long)ck.b * a.HK + ck.h) * D + dp * EPL;
     uint4 kr[U], vr[U];
     int row[U];
     bool valid[U];
+    float sold[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      row[u] = ti.ncache;
+      row[u] = ck.ncache;
       valid[u] = (u == 0) && (rg == 0);
+      sold[u] = 0.0f;
       kr[u] = *reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(a.k_new) + nb);
       vr[u] = *reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(a.v_new) + nb);
     }
     if (rg == 0) {
-      *reinterpret_cast<uint4*>(reinterpret_cast<float*>(a.k_w) + (ti.segrow0 + ti.ncache) * D + dp * EPL) = kr[0];
-      *reinterpret_cast<uint4*>(reinterpret_cast<float*>(a.v_w) + (ti.segrow0 + ti.ncache) * D + dp * EPL) = vr[0];
+      *reinterpret_cast<uint4*>(reinterpret_cast<float*>(a.k_w) + (ck.segrow0 + ck.ncache) * D + dp * EPL) = kr[0];
+      *reinterpret_cast<uint4*>(reinterpret_cast<float*>(a.v_w) + (ck.segrow0 + ck.ncache) * D + dp * EPL) = vr[0];
     }
-    consume(kr, vr, row, valid);
+    if (lane == 0) pd.score[ck.ncache] = 0.0f;
+    consume(kr, vr, valid, false, row, sold);
   }
 #pragma unroll
   for (int off = LPR; off < kWave; off <<= 1) {
@@ -530,11 +598,10 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const PlanLds& P, CombineLds
       }
     }
   }
-  write_partial<D, G>(a, cb, t);
 }
 
 // ---------------------------------------------------------------------------
-// Kernels
+// Kernel
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 struct AttnLds;
@@ -545,6 +612,7 @@ struct AttnLds<bf16_t, D> {
     char vtiles[kNumWaves * MfmaCfg<D>::TILE_BYTES];
     CombineLds cb;
   };
+  QLds<D> qs;
 };
 
 template <int D>
@@ -553,127 +621,187 @@ struct AttnLds<float, D> {
 };
 
 template <typename T, int D, int G>
-__global__ __launch_bounds__(kThreads) void attn_kernel(DecodeArgs a) {
-  __shared__ PlanLds P;
-  __shared__ __attribute__((aligned(16))) AttnLds<T, D> L;
+__device__ inline void decode_body(const DecodeArgs& a) {
+  __shared__ __attribute__((aligned(16))) AttnLds<T, D> S;
+  __shared__ int s_last;
   const int tid = threadIdx.x;
-  if (tid < kWave) make_plan(a, P);
-  __syncthreads();
-  const int t = blockIdx.x;
-  if (t == 0) {
-    // Publish the plan for the finalize kernel.
-    int* pl = a.plan;
-    for (int b = tid; b < a.B; b += kThreads) {
-      pl[kPlanHdr + b] = P.n_att[b];
-      pl[kPlanHdr + kMaxSeqs + b] = P.flag[b];
+  const int seg = blockIdx.x / a.nch;
+  const int c = blockIdx.x - seg * a.nch;
+  const int b = seg / a.HK;
+  const int h = seg - b * a.HK;
+  const int HQ = a.HK * G;
+
+  const int n = a.len[b];
+  const int cp = a.cap[b];
+  const long long sbase = a.seq_base[b];
+  const bool app = a.k_new != nullptr;
+  const bool bad = n < 0 || cp < 0 || n > cp || sbase < 0 || sbase + (long long)a.HK * cp > a.rows_per_layer;
+  const bool ovf = !bad && app && n >= cp;
+  const int n_att = (bad || ovf) ? 0 : n + (app ? 1 : 0);
+  if (n_att == 0) {
+    // Skipped (flagged) or empty sequence: its out rows get NaN or 0, nothing
+    // else of it changes, and no counter is touched.
+    if (c == 0) {
+      const float fill = (bad || ovf) ? __int_as_float(0x7fc00000) : 0.0f;
+      float* ob = a.out + ((long long)b * HQ + (long long)h * G) * D;
+      for (int i = tid; i < G * D; i += kThreads) ob[i] = fill;
+      if (h == 0 && tid == 0 && (bad || ovf))
+        atomic_or_status(a.dev_status, bad ? LETHE_DEV_BAD_LAYOUT : LETHE_DEV_APPEND_OVERFLOW);
     }
-    if (tid == 0) {
-      pl[kPlanC] = P.C;
-      pl[kPlanTasks] = P.tasks;
-    }
+    return;
   }
-  if (t >= P.tasks) return;
-  if constexpr (sizeof(T) == 2)
-    attn_chunk_mfma<D, G>(a, P, L.vtiles, L.cb, t);
-  else
-    attn_chunk_f32<D, G>(a, P, L.cb, t);
+  int csz = (n_att + a.nch - 1) / a.nch;
+  csz = ((csz + 31) / 32) * 32;
+  if (csz < a.min_chunk) csz = a.min_chunk;
+  const int nne = (n_att + csz - 1) / csz;  // chunks with rows
+  const int par = a.pend_par[b] & 1;
+  const size_t qgroup = ((size_t)b * HQ + (size_t)h * G) * D * sizeof(T);  // bytes
+  const size_t qhalf = (size_t)a.B * HQ * D * sizeof(T);
+
+  Chunk ck;
+  ck.b = b;
+  ck.h = h;
+  ck.seg = seg;
+  ck.c = c;
+  ck.r0 = c * csz;
+  ck.r1 = min(ck.r0 + csz, n_att);
+  ck.app = app;
+  ck.ncache = n;
+  ck.segrow0 = sbase + (long long)h * cp;
+  const int ps = part_stride(G, D);
+
+  if (c == 0) {
+    // Keep this step's queries of the group for the next call's score update.
+    const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.q) + qgroup);
+    uint4* dst = reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.qprev) + (par ^ 1) * qhalf + qgroup);
+    for (int i = tid; i < (int)(G * D * sizeof(T) / 16); i += kThreads) dst[i] = src[i];
+  }
+  if (c < nne) {
+    Pending<G> pd;
+    const int pl = a.pend_len[b];
+    pd.rows = pl > 0 ? min(pl, n) : 0;
+    pd.score = a.score + ck.segrow0;
+    pd.stat = a.segstat + (long long)seg * 2 * G;
+    pd.q = reinterpret_cast<const char*>(a.qprev) + par * qhalf + qgroup;
+    pd.gamma = a.pend_gamma[b];
+    pd.scale = a.pend_scale[b];
+    if constexpr (sizeof(T) == 2)
+      attn_chunk_mfma<D, G>(a, ck, pd, S.vtiles, S.qs, S.cb);
+    else
+      attn_chunk_f32<D, G>(a, ck, pd, S.cb);
+    write_partial<D, G>(S.cb, a.part + ((long long)seg * a.nch + c) * ps);
+  }
+
+  // Completion count: every block of the segment, with or without rows.
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0)
+    s_last = __hip_atomic_fetch_add(&a.seg_cnt[(long long)seg * kCntStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.nch - 1;
+  __syncthreads();
+  if (!s_last) return;
+
+  // Every block of this segment has read len and the pending state.
+  int seq_done = 0;
+  if (tid == 0) {
+    __hip_atomic_store(&a.seg_cnt[(long long)seg * kCntStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    seq_done = __hip_atomic_fetch_add(&a.seq_cnt[(long long)b * kCntStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.HK - 1;
+  }
+  combine_segment<D, G>(a, ck, nne);
+  if (seq_done) {
+    // ... and so has every block of the sequence.
+    if (app) a.len[b] = n_att;
+    a.pend_len[b] = n_att;
+    a.pend_par[b] = par ^ 1;
+    a.pend_gamma[b] = a.gamma;
+    a.pend_scale[b] = a.scale_log2;
+    __hip_atomic_store(&a.seq_cnt[(long long)b * kCntStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
-struct FinLds {
-  PlanLds P;
-  float M[8];
-  float invL[8];
-};
+// bf16: three resident blocks per CU need at most 168 registers per lane.
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void decode_bf16_kernel(DecodeArgs a) {
+  decode_body<bf16_t, D, G>(a);
+}
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void finalize_kernel(DecodeArgs a) {
-  __shared__ FinLds F;
-  const int tid = threadIdx.x;
-  const int* pl = a.plan;
-  const int t = blockIdx.x;
-  const int tasks = pl[kPlanTasks];
-  if (t >= tasks && t != 0) return;
-  for (int b = tid; b < a.B; b += kThreads) {
-    F.P.n_att[b] = pl[kPlanHdr + b];
-    F.P.flag[b] = (unsigned char)pl[kPlanHdr + kMaxSeqs + b];
-  }
-  __syncthreads();
-  if (tid < kWave) plan_chunks(a, F.P, pl[kPlanC]);
-  __syncthreads();
+__global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
+  decode_body<float, D, G>(a);
+}
+
+template <typename T, int D, int G>
+constexpr auto decode_kernel() {
+  if constexpr (sizeof(T) == 2)
+    return decode_bf16_kernel<D, G>;
+  else
+    return decode_f32_kernel<D, G>;
+}
+
+// ---------------------------------------------------------------------------
+// Flush: apply the pending step of every (layer, sequence), block per
+// (layer, sequence, KV head); a second kernel clears the pending lengths.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
+  constexpr int EPL = Elem<T>::kPer16B;
+  constexpr int LPR = D / EPL;
+  constexpr int RPW = kWave / LPR;
+  const int lb = blockIdx.x / a.HK;
+  const int h = blockIdx.x - lb * a.HK;
+  const int l = lb / a.B;
+  const int b = lb - l * a.B;
+  const int P = a.pend_len[lb];
+  if (P <= 0) return;
+  const int n = a.len[lb];
+  const int cp = a.cap[b];
+  const long long sbase = a.seq_base[b];
+  if (n < 0 || cp < 0 || n > cp || sbase < 0 || sbase + (long long)a.HK * cp > a.rows_per_layer) return;
+  const int rows = min(P, n);
+  const int par = a.pend_par[lb] & 1;
+  const float gamma = a.pend_gamma[lb];
+  const float scale = a.pend_scale[lb];
   const int HQ = a.HK * G;
-  if (t == 0) {
-    for (int b = tid; b < a.B; b += kThreads)
-      if (F.P.flag[b] & kFlagAppended) a.len[b] = F.P.n_att[b];
-    int fl = 0;
-    for (int b = tid; b < a.B; b += kThreads) fl |= F.P.flag[b] & (kFlagOverflow | kFlagBad);
-    atomic_or_status(a.dev_status, fl);
-    for (int b = 0; b < a.B; ++b) {
-      if (F.P.n_att[b] != 0) continue;
-      const float fill = (F.P.flag[b] & (kFlagOverflow | kFlagBad)) ? __int_as_float(0x7fc00000) : 0.0f;
-      float* ob = a.out + (long long)b * HQ * D;
-      for (int i = tid; i < HQ * D; i += kThreads) ob[i] = fill;
-    }
-  }
-  if (t >= tasks) return;
-  const TaskInfo ti = task_info(a, F.P, t);
-  const int lane = tid & (kWave - 1);
-  const int w = tid / kWave;
-  const float* part0 = a.part + (long long)(F.P.base[ti.b] + ti.h * ti.nc) * G * (D + 2);
-  for (int g = w; g < G; g += kNumWaves) {
-    float mx = kNegBig;
-    for (int cc = lane; cc < ti.nc; cc += kWave) mx = fmaxf(mx, part0[(long long)cc * G * (D + 2) + g * (D + 2)]);
-    mx = wave_max(mx);
-    float ls = 0.0f;
-    for (int cc = lane; cc < ti.nc; cc += kWave) {
-      const float* p = part0 + (long long)cc * G * (D + 2) + g * (D + 2);
-      ls += p[1] * exp2f(p[0] - mx);
-    }
-    ls = wave_sum(ls);
-    if (lane == 0) {
-      F.M[g] = mx;
-      F.invL[g] = 1.0f / ls;
-    }
-  }
-  __syncthreads();
-  // Scores of the chunk's rows.
-  const float* pend = a.pend + ti.segrow0 * G;
-  float* score = a.score + ti.segrow0;
-  for (int r = ti.r0 + tid; r < ti.r1; r += kThreads) {
-    float acc = 0.0f;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x / kWave;
+  const int rg = lane / LPR;
+  const int dp = lane % LPR;
+  const long long segrow0 = (long long)l * a.rows_per_layer + sbase + (long long)h * cp;
+  const T* qg = reinterpret_cast<const T*>(a.qprev) + (((long long)l * 2 + par) * a.B + b) * HQ * D + (long long)h * G * D;
+  const float* st = a.segstat + ((long long)lb * a.HK + h) * 2 * G;
+  float qf[G][EPL], M[G], iL[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) acc += exp2f(pend[(long long)r * G + g] - F.M[g]) * F.invL[g];
-    const float s_old = (r < ti.ncache) ? score[r] : 0.0f;
-    score[r] = fmaf(a.gamma, s_old, acc);
+  for (int g = 0; g < G; ++g) {
+    Elem<T>::unpack(*reinterpret_cast<const uint4*>(qg + (long long)g * D + dp * EPL), qf[g]);
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) qf[g][e] *= scale;
+    M[g] = st[g];
+    iL[g] = st[G + g];
   }
-  // One slice of the segment's output: elements [e0, e1) of its G x D block.
-  const int per = (G * D + ti.nc - 1) / ti.nc;
-  const int e0 = ti.c * per, e1 = min(e0 + per, G * D);
-  float* outb = a.out + ((long long)ti.b * HQ + (long long)ti.h * G) * D;
-  for (int e = e0 + tid; e < e1; e += kThreads) {
-    const int g = e / D, d = e % D;
-    const float Mg = F.M[g];
-    float acc = 0.0f;
-    int cc = 0;
-    for (; cc + 4 <= ti.nc; cc += 4) {
-      float mv[4], ov[4];
+  const T* Kb = reinterpret_cast<const T*>(a.k) + segrow0 * D + dp * EPL;
+  float* score = a.score + segrow0;
+  for (int r0 = w * RPW; r0 < rows; r0 += kNumWaves * RPW) {
+    const int r = r0 + rg;
+    const int rr = min(r, rows - 1);
+    float kf[EPL];
+    Elem<T>::unpack(*reinterpret_cast<const uint4*>(Kb + (long long)rr * D), kf);
+    float c = 0.0f;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float* p = part0 + (long long)(cc + k) * G * (D + 2) + g * (D + 2);
-        mv[k] = p[0];
-        ov[k] = p[2 + d];
-      }
+    for (int g = 0; g < G; ++g) {
+      float acc = 0.0f;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) acc = fmaf(ov[k], exp2f(mv[k] - Mg), acc);
+      for (int e = 0; e < EPL; ++e) acc = fmaf(qf[g][e], kf[e], acc);
+      c = fmaf(exp2f(group_sum<LPR>(acc) - M[g]), iL[g], c);
     }
-    for (; cc < ti.nc; ++cc) {
-      const float* p = part0 + (long long)cc * G * (D + 2) + g * (D + 2);
-      acc = fmaf(p[2 + d], exp2f(p[0] - Mg), acc);
-    }
-    outb[e] = acc * F.invL[g];
+    if (dp == 0 && r < rows) score[r] = fmaf(gamma, score[r], c);
   }
 }
 
-// Optional tuning overrides, read once: LETHE_DECODE_TASKS (chunks to aim
+__global__ void flush_clear_kernel(int32_t* pend_len, int count) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) pend_len[i] = 0;
+}
+
+// Optional tuning overrides, read once: LETHE_DECODE_BLOCKS (blocks to aim
 // for per launch) and LETHE_DECODE_MIN_CHUNK (rows).
 int env_int(const char* name) {
   const char* v = getenv(name);
@@ -686,7 +814,7 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   // Resident blocks per device for this instantiation; the value depends only
   // on the device, so concurrent first calls store the same number.
   static int resident[64];
-  static const int env_tasks = env_int("LETHE_DECODE_TASKS");
+  static const int env_blocks = env_int("LETHE_DECODE_BLOCKS");
   static const int env_chunk = env_int("LETHE_DECODE_MIN_CHUNK");
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return LETHE_ERR_HIP;
@@ -694,18 +822,22 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   if (blocks <= 0) {
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return LETHE_ERR_HIP;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<T, D, G>, kThreads, 0) != hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<T, D, G>(), kThreads, 0) != hipSuccess)
       return LETHE_ERR_HIP;
     blocks = cus * (per_cu < 1 ? 1 : per_cu);
     if (dev >= 0 && dev < 64) __atomic_store_n(&resident[dev], blocks, __ATOMIC_RELAXED);
   }
-  a.target_tasks = env_tasks > 0 ? env_tasks : blocks;
-  if (a.target_tasks > kMaxDecodeTasks) a.target_tasks = kMaxDecodeTasks;
-  a.min_chunk = env_chunk > 0 ? ((env_chunk + 63) / 64) * 64 : 256;
-  const int grid = a.target_tasks + a.B * a.HK;  // upper bound on the chunk count
-  hipLaunchKernelGGL((attn_kernel<T, D, G>), dim3(grid), dim3(kThreads), 0, s, a);
-  if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
-  hipLaunchKernelGGL((finalize_kernel<D, G>), dim3(grid), dim3(kThreads), 0, s, a);
+  const int target = env_blocks > 0 ? env_blocks : blocks;
+  const int64_t segs = (int64_t)a.B * a.HK;
+  int64_t nch = target / segs;
+  const int64_t cap_nch = decode_max_chunks(a.B, a.HK) / segs;
+  if (nch > cap_nch) nch = cap_nch;
+  if (nch > kMaxChunksPerSeg) nch = kMaxChunksPerSeg;
+  if (nch < 1) nch = 1;
+  a.nch = (int32_t)nch;
+  a.min_chunk = env_chunk > 0 ? ((env_chunk + 31) / 32) * 32 : 128;
+  const auto kernel = decode_kernel<T, D, G>();
+  hipLaunchKernelGGL(kernel, dim3((unsigned)(segs * nch)), dim3(kThreads), 0, s, a);
   if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
   return LETHE_OK;
 }
@@ -725,6 +857,30 @@ lethe_status launch_td(const DecodeArgs& a, int G, hipStream_t s) {
   return LETHE_ERR_UNSUPPORTED;
 }
 
+template <typename T, int D, int G>
+lethe_status launch_flush_tdg(const FlushArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((flush_kernel<T, D, G>), dim3((unsigned)(a.L * a.B * a.HK)), dim3(kThreads), 0, s, a);
+  if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
+  const int count = a.L * a.B;
+  hipLaunchKernelGGL(flush_clear_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, a.pend_len, count);
+  return hipGetLastError() == hipSuccess ? LETHE_OK : LETHE_ERR_HIP;
+}
+
+template <typename T, int D>
+lethe_status launch_flush_td(const FlushArgs& a, int G, hipStream_t s) {
+  switch (G) {
+    case 1: return launch_flush_tdg<T, D, 1>(a, s);
+    case 2: return launch_flush_tdg<T, D, 2>(a, s);
+    case 3: return launch_flush_tdg<T, D, 3>(a, s);
+    case 4: return launch_flush_tdg<T, D, 4>(a, s);
+    case 5: return launch_flush_tdg<T, D, 5>(a, s);
+    case 6: return launch_flush_tdg<T, D, 6>(a, s);
+    case 7: return launch_flush_tdg<T, D, 7>(a, s);
+    case 8: return launch_flush_tdg<T, D, 8>(a, s);
+  }
+  return LETHE_ERR_UNSUPPORTED;
+}
+
 }  // namespace
 
 lethe_status launch_decode(const DecodeArgs& a, lethe_dtype dt, int D, int G, hipStream_t s) {
@@ -734,6 +890,17 @@ lethe_status launch_decode(const DecodeArgs& a, lethe_dtype dt, int D, int G, hi
   } else {
     if (D == 128) return launch_td<float, 128>(a, G, s);
     if (D == 64) return launch_td<float, 64>(a, G, s);
+  }
+  return LETHE_ERR_UNSUPPORTED;
+}
+
+lethe_status launch_flush(const FlushArgs& a, lethe_dtype dt, int D, int G, hipStream_t s) {
+  if (dt == LETHE_BF16) {
+    if (D == 128) return launch_flush_td<bf16_t, 128>(a, G, s);
+    if (D == 64) return launch_flush_td<bf16_t, 64>(a, G, s);
+  } else {
+    if (D == 128) return launch_flush_td<float, 128>(a, G, s);
+    if (D == 64) return launch_flush_td<float, 64>(a, G, s);
   }
   return LETHE_ERR_UNSUPPORTED;
 }

@@ -11,11 +11,9 @@ namespace {
 
 size_t elem_bytes(lethe_dtype dt) { return dt == LETHE_BF16 ? 2 : 4; }
 
-// Host-checkable validity of a cache description.
-lethe_status check_cache(const lethe_cache* c) {
+// Host-checkable validity of the sizes of a cache description.
+lethe_status check_desc(const lethe_cache* c) {
   if (!c) return LETHE_ERR_INVALID;
-  if (!c->k || !c->v || !c->score || !c->len || !c->seq_base || !c->cap || !c->dev_status)
-    return LETHE_ERR_INVALID;
   if (c->num_layers < 1 || c->num_seqs < 1 || c->num_q_heads < 1 || c->num_kv_heads < 1)
     return LETHE_ERR_INVALID;
   if (c->rows_per_layer < 1) return LETHE_ERR_INVALID;
@@ -29,6 +27,44 @@ lethe_status check_cache(const lethe_cache* c) {
   // Element offsets must stay within int64 and row indices within 2^40.
   if (c->rows_per_layer > ((int64_t)1 << 40) / c->num_layers) return LETHE_ERR_UNSUPPORTED;
   return LETHE_OK;
+}
+
+// Sizes plus the device pointers every call needs.
+lethe_status check_cache(const lethe_cache* c) {
+  lethe_status st = check_desc(c);
+  if (st != LETHE_OK) return st;
+  if (!c->k || !c->v || !c->score || !c->len || !c->seq_base || !c->cap || !c->dev_status || !c->state)
+    return LETHE_ERR_INVALID;
+  return LETHE_OK;
+}
+
+int group_size(const lethe_cache* c) { return c->num_q_heads / c->num_kv_heads; }
+
+StateLayout state_of(const lethe_cache* c) {
+  return state_layout(c->num_layers, c->num_seqs, c->num_kv_heads, group_size(c), c->head_dim, elem_bytes(c->dtype));
+}
+
+// Applies every pending decode step (no-op kernel blocks where none is).
+lethe_status flush_pending(const lethe_cache* c, hipStream_t stream) {
+  const StateLayout sl = state_of(c);
+  char* st = (char*)c->state;
+  FlushArgs a;
+  a.k = c->k;
+  a.score = c->score;
+  a.len = c->len;
+  a.seq_base = c->seq_base;
+  a.cap = c->cap;
+  a.rows_per_layer = c->rows_per_layer;
+  a.L = c->num_layers;
+  a.B = c->num_seqs;
+  a.HK = c->num_kv_heads;
+  a.pend_len = (int32_t*)(st + sl.len_off);
+  a.pend_par = (const int32_t*)(st + sl.par_off);
+  a.pend_gamma = (const float*)(st + sl.gamma_off);
+  a.pend_scale = (const float*)(st + sl.scale_off);
+  a.segstat = (const float*)(st + sl.stat_off);
+  a.qprev = st + sl.q_off;
+  return launch_flush(a, c->dtype, c->head_dim, group_size(c), stream);
 }
 
 }  // namespace
@@ -47,11 +83,10 @@ const char* lethe_status_string(lethe_status s) {
 }
 
 size_t lethe_workspace_bytes(const lethe_cache* c, int op) {
-  if (check_cache(c) != LETHE_OK) return 0;
-  int G = c->num_q_heads / c->num_kv_heads;
+  if (check_desc(c) != LETHE_OK) return 0;
   switch (op) {
     case LETHE_OP_DECODE:
-      return decode_ws_layout(c->num_seqs, c->num_kv_heads, G, c->head_dim, c->rows_per_layer).total;
+      return decode_ws_bytes(c->num_seqs, c->num_kv_heads, group_size(c), c->head_dim);
     case LETHE_OP_SPARSITY:
       return 0;
     case LETHE_OP_SELECT:
@@ -60,6 +95,17 @@ size_t lethe_workspace_bytes(const lethe_cache* c, int op) {
       return align_up((size_t)c->num_layers * c->num_seqs * c->num_kv_heads * sizeof(int32_t), 256);
   }
   return 0;
+}
+
+size_t lethe_state_bytes(const lethe_cache* c) {
+  if (check_desc(c) != LETHE_OK) return 0;
+  return state_of(c).total;
+}
+
+lethe_status lethe_score_flush(const lethe_cache* c, hipStream_t stream) {
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  return flush_pending(c, stream);
 }
 
 lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const void* q,
@@ -73,10 +119,9 @@ lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const 
   if ((k_new == nullptr) != (v_new == nullptr)) return LETHE_ERR_INVALID;
   if (!(gamma > 0.0f && gamma <= 1.0f)) return LETHE_ERR_INVALID;  // also rejects NaN
   if (isnan(softmax_scale) || isinf(softmax_scale)) return LETHE_ERR_INVALID;
-  const int G = c->num_q_heads / c->num_kv_heads;
+  const int G = group_size(c);
   const int D = c->head_dim;
-  DecodeWs w = decode_ws_layout(c->num_seqs, c->num_kv_heads, G, D, c->rows_per_layer);
-  if (ws_bytes < w.total) return LETHE_ERR_WORKSPACE;
+  if (ws_bytes < decode_ws_bytes(c->num_seqs, c->num_kv_heads, G, D)) return LETHE_ERR_WORKSPACE;
   float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)D);
 
   const size_t eb = elem_bytes(c->dtype);
@@ -99,11 +144,20 @@ lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const 
   a.scale_log2 = scale * 1.4426950408889634f;
   a.gamma = gamma;
   a.out = out;
-  a.plan = (int32_t*)((char*)ws + w.plan_off);
-  a.part = (float*)((char*)ws + w.part_off);
-  a.pend = (float*)((char*)ws + w.pend_off);
+  const StateLayout sl = state_of(c);
+  char* st_base = (char*)c->state;
+  const size_t lb = (size_t)layer * c->num_seqs;
+  a.pend_len = (int32_t*)(st_base + sl.len_off) + lb;
+  a.pend_par = (int32_t*)(st_base + sl.par_off) + lb;
+  a.pend_gamma = (float*)(st_base + sl.gamma_off) + lb;
+  a.pend_scale = (float*)(st_base + sl.scale_off) + lb;
+  a.segstat = (float*)(st_base + sl.stat_off) + lb * c->num_kv_heads * 2 * G;
+  a.qprev = st_base + sl.q_off + lb * 2 * (size_t)c->num_q_heads * D * eb;
+  a.seg_cnt = (int32_t*)(st_base + sl.seg_cnt_off);
+  a.seq_cnt = (int32_t*)(st_base + sl.seq_cnt_off);
+  a.part = (float*)ws;
   a.dev_status = c->dev_status;
-  a.target_tasks = 0;  // chosen by the launcher
+  a.nch = 0;  // chosen by the launcher
   a.min_chunk = 0;
   return launch_decode(a, c->dtype, D, G, stream);
 }
@@ -118,6 +172,8 @@ lethe_status lethe_layer_sparsity(const lethe_cache* c, const int64_t* global_bu
   if (st != LETHE_OK) return st;
   if (!global_budget || !sparsity_out || !budget_out) return LETHE_ERR_INVALID;
   if (recent < 0 || sink < 0) return LETHE_ERR_INVALID;
+  st = flush_pending(c, stream);
+  if (st != LETHE_OK) return st;
   SparsityArgs a;
   a.score = c->score;
   a.len = c->len;
@@ -146,6 +202,8 @@ lethe_status lethe_rasr_select(const lethe_cache* c, const int32_t* budget, int3
   if (st != LETHE_OK) return st;
   if (!budget || !keep) return LETHE_ERR_INVALID;
   if (recent < 0 || sink < 0) return LETHE_ERR_INVALID;
+  st = flush_pending(c, stream);
+  if (st != LETHE_OK) return st;
   SelectArgs a;
   a.score = c->score;
   a.len = c->len;
@@ -169,6 +227,8 @@ lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* w
   if (st != LETHE_OK) return st;
   if (!keep || !ws) return LETHE_ERR_INVALID;
   if (ws_bytes < lethe_workspace_bytes(c, LETHE_OP_COMPACT)) return LETHE_ERR_WORKSPACE;
+  st = flush_pending(c, stream);
+  if (st != LETHE_OK) return st;
   CompactArgs a;
   a.k = c->k;
   a.v = c->v;

@@ -9,37 +9,73 @@
 
 namespace lethe {
 
-// Largest batch the decode planner keeps in LDS.
+// Largest batch (the budget kernel and the tests size arrays by it).
 constexpr int kMaxSeqs = 1024;
 // Largest number of layers the budget split handles.
 constexpr int kMaxLayers = 256;
-// Upper bounds on decode blocks and on the chunk target of one launch; the
-// workspace is sized for kMaxDecodeTasks + num_seqs * num_kv_heads chunks.
-constexpr int kMaxDecodeBlocks = 4096;
-constexpr int kMaxDecodeTasks = 8192;
+// Most chunks one (sequence, KV head) segment is split into per decode call
+// (also the lane count of the combine, one chunk per lane).
+constexpr int kMaxChunksPerSeg = 64;
+// Most chunks per decode call over all segments (sizes the partial buffer).
+constexpr int kMaxDecodeChunks = 8192;
 
-inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+__host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Decode workspace layout (bytes from ws); nothing in it needs to be
-// initialised, every word is written before it is read within a call:
-//   plan   header (chunk rows, chunk count) + n_att[kMaxSeqs] + flag[kMaxSeqs]
-//   part   per chunk and head: m, l, o[D]
-//   pend   per row and head: scaled logit of the current step
-struct DecodeWs {
-  size_t plan_off, part_off, pend_off, total;
+// Per-cache decode state (lethe_cache::state), zero-filled once before first
+// use; the calls keep it consistent afterwards.
+//
+// The score update of a decode step needs the step's final softmax max and
+// sum per head, which exist only once every chunk of the segment is done.  A
+// decode call therefore leaves its step pending: it keeps the step's query
+// and scale and, per segment and head, (M, 1/L).  The next decode call on the
+// layer recomputes the pending step's logits from the K rows it streams
+// anyway and applies the update; a flush does the same on its own.
+//   pend_len   [L][B]               rows with a pending contribution (0: none)
+//   pend_par   [L][B]               which half of qprev holds the pending query
+//   pend_gamma [L][B]               decay of the pending step
+//   pend_scale [L][B]               softmax scale * log2(e) of the pending step
+//   seg_cnt    [B*HK] x kCntStride  blocks of a segment done (0 between calls)
+//   seq_cnt    [B] x kCntStride     segments of a sequence done (0 between calls)
+//   segstat    [L][B*HK][2G]        per head: M (max scaled logit), then 1 / L
+//   qprev      [L][2][B][HQ][D]     queries (storage type), double buffered
+// Counters sit kCntStride words apart so the atomics of different segments
+// meet in different cache lines and memory channels.
+constexpr int kCntStride = 64;
+
+struct StateLayout {
+  size_t len_off, par_off, gamma_off, scale_off, seg_cnt_off, seq_cnt_off, stat_off, q_off, total;
 };
 
-enum PlanField { kPlanC = 0, kPlanTasks = 1, kPlanHdr = 16 };
+inline StateLayout state_layout(int L, int B, int HK, int G, int D, size_t elem_bytes) {
+  StateLayout s;
+  const size_t lb = (size_t)L * B;
+  s.len_off = 0;
+  s.par_off = align_up(lb * sizeof(int32_t), 256);
+  s.gamma_off = s.par_off + align_up(lb * sizeof(int32_t), 256);
+  s.scale_off = s.gamma_off + align_up(lb * sizeof(float), 256);
+  s.seg_cnt_off = s.scale_off + align_up(lb * sizeof(float), 256);
+  s.seq_cnt_off = s.seg_cnt_off + align_up((size_t)B * HK * kCntStride * sizeof(int32_t), 256);
+  s.stat_off = s.seq_cnt_off + align_up((size_t)B * kCntStride * sizeof(int32_t), 256);
+  s.q_off = s.stat_off + align_up(lb * HK * 2 * G * sizeof(float), 256);
+  s.total = s.q_off + align_up(lb * 2 * (size_t)HK * G * D * elem_bytes, 256);
+  return s;
+}
 
-inline DecodeWs decode_ws_layout(int B, int HK, int G, int D, int64_t rows_per_layer) {
-  DecodeWs w;
-  const size_t segs = (size_t)B * HK;
-  const size_t max_chunks = (size_t)kMaxDecodeTasks + segs;
-  w.plan_off = 0;
-  w.part_off = align_up(sizeof(int32_t) * (kPlanHdr + 2 * (size_t)kMaxSeqs), 256);
-  w.pend_off = w.part_off + align_up(max_chunks * (size_t)G * (D + 2) * sizeof(float), 256);
-  w.total = w.pend_off + align_up((size_t)rows_per_layer * G * sizeof(float), 256);
-  return w;
+// Floats per chunk partial (m, l, o[D] per head), padded to 128 bytes so no
+// two chunks share a cache line.
+__host__ __device__ inline int part_stride(int G, int D) { return (int)align_up((size_t)G * (D + 2), 32); }
+
+// Chunks the partial buffer of a decode workspace holds.
+inline int64_t decode_max_chunks(int B, int HK) {
+  const int64_t segs = (int64_t)B * HK;
+  int64_t c = segs * kMaxChunksPerSeg;
+  if (c > kMaxDecodeChunks) c = kMaxDecodeChunks;
+  return c < segs ? segs : c;
+}
+
+// Decode workspace: the chunk partials, scratch between calls.
+inline size_t decode_ws_bytes(int B, int HK, int G, int D) {
+  return align_up((size_t)decode_max_chunks(B, HK) * part_stride(G, D) * sizeof(float), 256);
 }
 
 struct DecodeArgs {
@@ -59,13 +95,37 @@ struct DecodeArgs {
   float scale_log2;      // softmax scale * log2(e)
   float gamma;
   float* out;            // [B][HQ][D]
-  int32_t* plan;         // ws
-  float* part;
-  float* pend;
+  int32_t* pend_len;     // state of this layer: [B]
+  int32_t* pend_par;     // [B]
+  float* pend_gamma;     // [B]
+  float* pend_scale;     // [B]
+  float* segstat;        // [B*HK][2G]
+  void* qprev;           // [2][B][HQ][D]
+  int32_t* seg_cnt;      // [B*HK] x kCntStride
+  int32_t* seq_cnt;      // [B] x kCntStride
+  float* part;           // workspace
   int32_t* dev_status;
-  int32_t target_tasks;  // attention chunks to aim for (0: one per resident block)
-  int32_t min_chunk;     // smallest chunk, rows (0: default)
+  int32_t nch;           // chunks per segment, 1 .. kMaxChunksPerSeg
+  int32_t min_chunk;     // rows, multiple of 32
 };
+
+struct FlushArgs {
+  const void* k;         // all layers
+  float* score;
+  const int32_t* len;    // [L][B]
+  const int64_t* seq_base;
+  const int32_t* cap;
+  int64_t rows_per_layer;
+  int32_t L, B, HK;
+  int32_t* pend_len;     // state, all layers
+  const int32_t* pend_par;
+  const float* pend_gamma;
+  const float* pend_scale;
+  const float* segstat;
+  const void* qprev;
+};
+
+lethe_status launch_flush(const FlushArgs& a, lethe_dtype dt, int D, int G, hipStream_t s);
 
 lethe_status launch_decode(const DecodeArgs& a, lethe_dtype dt, int D, int G, hipStream_t s);
 

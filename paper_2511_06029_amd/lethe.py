@@ -16,8 +16,9 @@ BF16, F32 = 0, 1
 DEV_APPEND_OVERFLOW, DEV_INFEASIBLE, DEV_BAD_LAYOUT, DEV_HEAD_MISMATCH = 1, 2, 4, 8
 OP_DECODE, OP_SPARSITY, OP_SELECT, OP_COMPACT = 0, 1, 2, 3
 
-EXPORTED = ("lethe_workspace_bytes", "lethe_decode_attn_score", "lethe_layer_sparsity",
-            "lethe_rasr_select", "lethe_kv_compact", "lethe_status_string")
+EXPORTED = ("lethe_workspace_bytes", "lethe_state_bytes", "lethe_decode_attn_score",
+            "lethe_layer_sparsity", "lethe_rasr_select", "lethe_kv_compact", "lethe_score_flush",
+            "lethe_status_string")
 
 
 class CCache(ctypes.Structure):
@@ -28,7 +29,7 @@ class CCache(ctypes.Structure):
         ("rows_per_layer", ctypes.c_int64), ("num_layers", ctypes.c_int32),
         ("num_seqs", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
         ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
-        ("dev_status", ctypes.c_void_p),
+        ("dev_status", ctypes.c_void_p), ("state", ctypes.c_void_p),
     ]
 
 
@@ -53,6 +54,10 @@ def load():
         pc = ctypes.POINTER(CCache)
         lib.lethe_workspace_bytes.argtypes = [pc, ctypes.c_int]
         lib.lethe_workspace_bytes.restype = sz
+        lib.lethe_state_bytes.argtypes = [pc]
+        lib.lethe_state_bytes.restype = sz
+        lib.lethe_score_flush.argtypes = [pc, vp]
+        lib.lethe_score_flush.restype = ctypes.c_int
         lib.lethe_decode_attn_score.argtypes = [pc, i32, vp, vp, vp, ctypes.c_float, ctypes.c_float, vp, vp, sz, vp]
         lib.lethe_decode_attn_score.restype = ctypes.c_int
         lib.lethe_layer_sparsity.argtypes = [pc, vp, i32, i32, vp, vp, vp, vp, sz, vp]
@@ -93,8 +98,19 @@ def workspace_bytes(cache, op):
     return int(load().lethe_workspace_bytes(ctypes.byref(cache.c_struct()), int(op)))
 
 
+def state_bytes(cache):
+    return int(load().lethe_state_bytes(ctypes.byref(cache.c_struct())))
+
+
+def score_flush(cache, stream=None):
+    """lethe_score_flush: apply the pending decode step of every (layer, sequence)."""
+    _check("lethe_score_flush", load().lethe_score_flush(ctypes.byref(cache.c_struct()), _stream(stream)))
+
+
 def decode_attn_score(cache, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, stream=None):
-    """lethe_decode_attn_score: append (k_new/v_new may be None), attend, update scores."""
+    """lethe_decode_attn_score: append (k_new/v_new may be None), attend; the
+    score update of this step stays pending until the next call on the layer,
+    score_flush or a prune call."""
     st = load().lethe_decode_attn_score(ctypes.byref(cache.c_struct()), int(layer), _p(q), _p(k_new),
                                         _p(v_new), float(gamma), float(softmax_scale), _p(out), _p(ws),
                                         ws.numel() * ws.element_size(), _stream(stream))
@@ -157,13 +173,29 @@ class LetheCache:
         self.cap = torch.tensor(self.caps, dtype=torch.int32, device=device)
         self.dev_status = torch.zeros(1, dtype=torch.int32, device=device)
         self._c = None
+        desc = self._struct(0)
+        nstate = int(load().lethe_state_bytes(ctypes.byref(desc)))
+        if nstate == 0:
+            raise LetheError("lethe_state_bytes", ERR_UNSUPPORTED)
+        self.state = torch.zeros(nstate, dtype=torch.uint8, device=device)
+
+    def _struct(self, state_ptr):
+        return CCache(self.k.data_ptr(), self.v.data_ptr(), self.score.data_ptr(), self.len.data_ptr(),
+                      self.seq_base.data_ptr(), self.cap.data_ptr(), self.rows_per_layer, self.L, self.B,
+                      self.HQ, self.HK, self.D, self.dtype_code, self.dev_status.data_ptr(), state_ptr)
 
     def c_struct(self):
         if self._c is None:
-            self._c = CCache(self.k.data_ptr(), self.v.data_ptr(), self.score.data_ptr(), self.len.data_ptr(),
-                             self.seq_base.data_ptr(), self.cap.data_ptr(), self.rows_per_layer, self.L, self.B,
-                             self.HQ, self.HK, self.D, self.dtype_code, self.dev_status.data_ptr())
+            self._c = self._struct(self.state.data_ptr())
         return self._c
+
+    def flush(self, stream=None):
+        """Make ``score`` current (apply the pending decode step)."""
+        score_flush(self, stream)
+
+    def reset_state(self):
+        """Drop any pending decode step (after editing len / scores directly)."""
+        self.state.zero_()
 
     def seg_rows(self, b, h):
         """Row range of segment (., b, h) within a layer."""

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_entry_point():
 
 
 def make(**kw):
-    c = L.CCache(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4096, 2, 4, 32, 8, 128, L.BF16, FAKE)
+    c = L.CCache(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4096, 2, 4, 32, 8, 128, L.BF16, FAKE, FAKE)
     for k, v in kw.items():
         setattr(c, k, v)
     return c
@@ -52,11 +52,12 @@ def test_workspace_sizes():
     lib = L.load()
     c = make()
     w = lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_DECODE)
-    # plan + partials for (4096 + B*H_KV) chunks * G heads * (D + 2) floats
-    # + one fp32 logit per row and head
-    G, D, B, HK, R = 4, 128, 4, 8, 4096
-    assert w >= (4096 + B * HK) * G * (D + 2) * 4 + R * G * 4
+    # chunk partials: up to 64 chunks per segment, G heads * (m, l, o[D]) floats
+    G, D, B, HK = 4, 128, 4, 8
+    assert w >= B * HK * 64 * G * (D + 2) * 4
     assert w % 256 == 0
+    # device pointers are not looked at
+    assert lib.lethe_workspace_bytes(ctypes.byref(make(k=None, state=None)), L.OP_DECODE) == w
     assert lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_COMPACT) >= 2 * B * HK * 4
     assert lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_SELECT) == 0
     assert lib.lethe_workspace_bytes(ctypes.byref(c), 99) == 0
@@ -67,7 +68,8 @@ def test_workspace_sizes():
 @pytest.mark.parametrize("field,value,want", [
     ("k", None, L.ERR_INVALID), ("v", None, L.ERR_INVALID), ("score", None, L.ERR_INVALID),
     ("len", None, L.ERR_INVALID), ("seq_base", None, L.ERR_INVALID), ("cap", None, L.ERR_INVALID),
-    ("dev_status", None, L.ERR_INVALID), ("num_layers", 0, L.ERR_INVALID), ("num_seqs", 0, L.ERR_INVALID),
+    ("dev_status", None, L.ERR_INVALID), ("state", None, L.ERR_INVALID),
+    ("num_layers", 0, L.ERR_INVALID), ("num_seqs", 0, L.ERR_INVALID),
     ("num_q_heads", 30, L.ERR_INVALID), ("num_kv_heads", 0, L.ERR_INVALID),
     ("rows_per_layer", 0, L.ERR_INVALID), ("dtype", 7, L.ERR_INVALID),
     ("head_dim", 96, L.ERR_UNSUPPORTED), ("head_dim", 256, L.ERR_UNSUPPORTED),
@@ -121,11 +123,36 @@ def test_prune_argument_validation():
     assert lib.lethe_kv_compact(cc, FAKE, FAKE, need - 1, None) == L.ERR_WORKSPACE
 
 
+def test_state_sizes():
+    lib = L.load()
+    G, B, HQ, HK, D, Ly = 4, 4, 32, 8, 128, 2
+    n = lib.lethe_state_bytes(ctypes.byref(make()))
+    # double-buffered bf16 queries of the pending step, plus (M, 1/L) per
+    # segment and head, plus small per-sequence arrays
+    core = Ly * 2 * B * HQ * D * 2 + Ly * B * HK * 2 * G * 4
+    assert core <= n < core + (1 << 14)
+    assert n % 256 == 0
+    assert lib.lethe_state_bytes(ctypes.byref(make(state=None, k=None))) == n
+    assert lib.lethe_state_bytes(ctypes.byref(make(rows_per_layer=1 << 20))) == n
+    assert lib.lethe_state_bytes(ctypes.byref(make(dtype=L.F32))) > n
+    assert lib.lethe_state_bytes(ctypes.byref(make(head_dim=96))) == 0
+    assert lib.lethe_state_bytes(None) == 0
+
+
+def test_flush_validation():
+    lib = L.load()
+    assert lib.lethe_score_flush(None, None) == L.ERR_INVALID
+    assert lib.lethe_score_flush(ctypes.byref(make(state=None)), None) == L.ERR_INVALID
+    assert lib.lethe_score_flush(ctypes.byref(make(len=None)), None) == L.ERR_INVALID
+    assert lib.lethe_score_flush(ctypes.byref(make(head_dim=96)), None) == L.ERR_UNSUPPORTED
+
+
 def test_struct_layout_matches_header():
     # Offsets of the C struct on x86-64 / gfx950 (LP64): six pointers, one
-    # int64, six 32-bit fields, one pointer.
+    # int64, six 32-bit fields, two pointers.
     assert L.CCache.rows_per_layer.offset == 48
     assert L.CCache.num_layers.offset == 56
     assert L.CCache.dtype.offset == 76
     assert L.CCache.dev_status.offset == 80
-    assert ctypes.sizeof(L.CCache) == 88
+    assert L.CCache.state.offset == 88
+    assert ctypes.sizeof(L.CCache) == 96
