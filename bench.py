@@ -21,6 +21,7 @@ decode call and the CPU oracle's throughput on a bounded sample.
 """
 import argparse
 import ctypes
+import hashlib
 import json
 import math
 import os
@@ -31,6 +32,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# rocprofv3 counter summary of the decode kernel on this workload (FETCH_SIZE
+# and WRITE_SIZE runs); used for roofline.traffic while the kernel sources
+# still hash to the value recorded there.
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_bf16_kernel_llama8b_b8_traffic.md")
+KERNEL_SOURCES = ("paper_2511_06029_amd/csrc/decode_attn.hip", "paper_2511_06029_amd/csrc/lethe_internal.h",
+                  "paper_2511_06029_amd/csrc/device_common.h")
 
 
 def parse():
@@ -39,9 +46,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=15, help="timed prune intervals")
     ap.add_argument("--warmup", type=int, default=1, help="untimed prune intervals")
     ap.add_argument("--interval", type=int, default=None, help="decode steps per prune interval (512)")
-    ap.add_argument("--sample-every", type=int, default=16, help="decode steps between per-call event samples")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="first copy MIB MiB device-to-device 3 times (counter calibration runs)")
     return ap.parse_args()
 
 
@@ -100,6 +108,17 @@ def main():
     keep = torch.empty((Lyr, cache.rows_per_layer), dtype=torch.uint8, device=dev)
     gbud = torch.empty(B, dtype=torch.int64, device=dev)
     torch.cuda.synchronize()
+    if args.copy_probe > 0:
+        # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings
+        # calibrate the counters for the decode kernel in the same run.
+        src = torch.ones(args.copy_probe << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("copy probe: 3 x %d MiB device-to-device" % args.copy_probe)
 
     lib = L.load()
     cref = ctypes.byref(cache.c_struct())
@@ -112,9 +131,6 @@ def main():
     v_ptr = [[ctypes.c_void_p(vp[t, l].data_ptr()) for l in range(Lyr)] for t in range(P)]
 
     len_snap = [torch.empty((Lyr, B), dtype=torch.int32, pin_memory=True) for _ in range(windows + 1)]
-    n_samples = args.steps * ((interval + args.sample_every - 1) // args.sample_every) * Lyr
-    call_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_samples)]
-    call_meta = []
     win_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(windows)]
 
     def run_window(w, timed):
@@ -123,15 +139,8 @@ def main():
         win_ev[w][0].record(stream)
         for i in range(interval):
             t = (w * interval + i) % P
-            sample = timed and (i % args.sample_every == 0)
             for l in range(Lyr):
-                if sample:
-                    e0, e1 = call_ev[len(call_meta)]
-                    e0.record(stream)
                 rc = fn(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, ws_p, wsb, sp)
-                if sample:
-                    e1.record(stream)
-                    call_meta.append((w, i, l))
                 if rc != 0:
                     raise RuntimeError("lethe_decode_attn_score: %s" % L.status_string(rc))
         win_ev[w][1].record(stream)
@@ -170,15 +179,14 @@ def main():
     elapsed = t1 - t0
     decode_ms = [win_ev[w][0].elapsed_time(win_ev[w][1]) for w in range(args.warmup, windows)]
     prune_ms = [win_ev[w][1].elapsed_time(win_ev[w][2]) for w in range(args.warmup, windows)]
-    # Per-call roofline of lethe_decode_attn_score (events on the launch stream).
-    call_ms, call_bytes = [], []
-    for (e0, e1), (w, i, l) in zip(call_ev, call_meta):
-        call_ms.append(e0.elapsed_time(e1))
-        n = len_snap[w].numpy()[l].astype(np.int64) + i + 1
-        call_bytes.append(int(n.sum()) * row_bytes + fixed_bytes)
-    avg_call_s = float(np.mean(call_ms)) / 1e3
-    avg_call_bytes = float(np.mean(call_bytes))
+    # Roofline of lethe_decode_attn_score: one kernel launch per call, back to
+    # back on the launch stream; the events bracket every decode call of the
+    # timed intervals, so their span / calls is the average launch duration.
+    n_calls = args.steps * interval * Lyr
+    avg_call_s = float(np.sum(decode_ms)) / 1e3 / n_calls
+    avg_call_bytes = (tokens * row_bytes + n_calls * fixed_bytes) / n_calls
     achieved = avg_call_bytes / avg_call_s / 1e9
+    traffic = load_traffic(avg_call_bytes)
 
     value = tokens / elapsed
     result = {
@@ -205,9 +213,10 @@ def main():
         "decode_hbm_gbs": achieved,
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic and traffic["bytes"],
             "kernel": "decode_bf16_kernel<128, 4> (lethe_decode_attn_score, one launch per layer call)",
-            "bytes_per_launch": avg_call_bytes, "launches_sampled": len(call_ms),
+            "bytes_per_launch": avg_call_bytes, "launches": n_calls,
+            "traffic_source": traffic and traffic["source"],
         },
         "final_lengths_mean": float(len_snap[windows].numpy().mean()),
     }
@@ -215,6 +224,39 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cache, args.cpu_seconds, gamma, log)
     print(json.dumps(result), flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def load_traffic(bytes_per_launch):
+    """HBM bytes per launch from the committed counter summary, scaled from
+    its run's algorithmic bytes per launch to this run's; None when there is
+    no summary or the kernel sources changed since it was taken."""
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    vals = {}
+    for line in text.splitlines():
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    try:
+        if vals["source_sha256"] != kernel_source_hash():
+            return None
+        measured = float(vals["hbm_bytes_per_launch"])
+        algorithmic = float(vals["algorithmic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+    return {"bytes": measured / algorithmic * bytes_per_launch,
+            "source": "%s (ratio %.4f of algorithmic bytes)" % (os.path.relpath(TRAFFIC_PROFILE, ROOT),
+                                                                measured / algorithmic)}
 
 
 def cpu_baseline(cache, budget_s, gamma, log):

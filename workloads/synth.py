@@ -181,8 +181,8 @@ class ZipfCache:
             for bb in range(cfg.batch):
                 z = torch.randn((cfg.num_kv_heads, cfg.head_dim, E), generator=self._gen(10, l, bb),
                                 device=self.device, dtype=torch.float32)
-                qm, _ = torch.linalg.qr(z)
-                us.append(qm.transpose(1, 2).contiguous())
+                qm, _ = torch.linalg.qr(z.cpu().double())  # small; LAPACK on the host
+                us.append(qm.float().to(self.device).transpose(1, 2).contiguous())
             self._dirs[l] = torch.stack(us)
         return self._dirs[l] if b is None else self._dirs[l][b]
 
