@@ -22,12 +22,14 @@
 //    more MFMA chain, Q_prev K^T) and applies
 //        s <- gamma s + sum_g exp2(x_g - M_g) / L_g
 //    to those rows.  launch_flush applies a pending step on its own.
-//  - The chunk's (m, l, o) partial goes to the workspace with write-through
-//    stores, then the block bumps its segment's counter.  The last block of a
-//    segment bumps the sequence's counter (the last segment of a sequence
-//    publishes its new length and pending step: every block of the sequence
-//    has read them by then) and combines the partials into out and the step's
-//    (M, 1/L) per head.  Counters go back to zero.
+//  - Every block bumps its sequence's counter once it has read len and the
+//    pending state; the last one publishes the new length and pending step
+//    (nobody of this launch reads them afterwards).
+//  - With one chunk per segment the block writes out and the step's (M, 1/L)
+//    per head itself.  Otherwise the chunk's (m, l, o) partial goes to the
+//    workspace with write-through stores, then the block bumps its segment's
+//    counter; the last block of a segment combines the partials.  Counters go
+//    back to zero.
 #include <math.h>
 #include <stdlib.h>
 
@@ -48,6 +50,8 @@ typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
 typedef __attribute__((address_space(3))) char lds_char_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) const void global_cvoid_t;
 
 // Write-through store and coherent load of two floats exchanged between the
 // blocks of one launch (relaxed, agent scope: no cache maintenance, no
@@ -115,6 +119,35 @@ __device__ void write_partial(const CombineLds& cb, float* part) {
   }
 }
 
+// A segment in one chunk: out and (M, 1/L) per head straight from the
+// per-wave states (the same arithmetic as a one-chunk combine).
+template <int D, int G>
+__device__ void finish_single(const DecodeArgs& a, const Chunk& ck, const CombineLds& cb) {
+  __syncthreads();
+  float* stat = a.segstat + (long long)ck.seg * 2 * G;
+  float* outb = a.out + ((long long)ck.b * a.HK * G + (long long)ck.h * G) * D;
+  for (int i = threadIdx.x; i < G * D / 2; i += kThreads) {
+    const int g = (2 * i) / D, d = (2 * i) % D;
+    float mx = kNegBig;
+#pragma unroll
+    for (int k = 0; k < kNumWaves; ++k) mx = fmaxf(mx, cb.m[k][g]);
+    float lsum = 0.0f, o0 = 0.0f, o1 = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kNumWaves; ++k) {
+      const float f = exp2f(cb.m[k][g] - mx);
+      lsum += cb.l[k][g] * f;
+      o0 += cb.o[k][g][d] * f;
+      o1 += cb.o[k][g][d + 1] * f;
+    }
+    const float inv = 1.0f / lsum;
+    *reinterpret_cast<float2*>(outb + g * D + d) = make_float2(o0 * inv, o1 * inv);
+    if (d == 0) {
+      stat[g] = mx;
+      stat[G + g] = inv;
+    }
+  }
+}
+
 // Last block of a segment: out and (M, 1/L) per head from the nne partials,
 // merged in batches of up to 16 chunks with online rescaling.
 template <int D, int G>
@@ -164,17 +197,24 @@ __device__ void combine_segment(const DecodeArgs& a, const Chunk& ck, int nne) {
 // ---------------------------------------------------------------------------
 // bf16 path on the matrix cores
 // ---------------------------------------------------------------------------
+// V rows reach LDS by direct loads (global_load_lds_dwordx4: lane l's 16
+// bytes land at base + 16 l).  Load u of a step carries rows u + VLOADS j
+// (j < RPL, LPR lanes per row) into block u; blocks are 1 KB plus 32 bytes
+// of padding, so the four rows one 16-lane group reads together in the
+// transposing read sit 8 banks apart.
 template <int D>
 struct MfmaCfg {
   static constexpr int KK = D / 32;          // k-steps of 32 over the head dim
   static constexpr int NT = D / 16;          // output tiles of 16 dims
   static constexpr int ROWB = D * 2;         // bytes per row
-  static constexpr int VSTRIDE = ROWB + 32;  // padded LDS row, bytes
   static constexpr int STEP = 32;            // rows per wavefront step
   static constexpr int LPR = ROWB / 16;      // lanes per row for V loads
   static constexpr int RPL = kWave / LPR;    // rows per V load
-  static constexpr int VLOADS = STEP / RPL;
-  static constexpr int TILE_BYTES = STEP * VSTRIDE;
+  static constexpr int VLOADS = STEP / RPL;  // loads (LDS blocks) per step
+  static constexpr int VBLK = kWave * 16 + 32;
+  static constexpr int TILE_BYTES = VLOADS * VBLK;
+  // LDS byte offset of row r (of the step), byte c of the row
+  static __device__ constexpr int vaddr(int r, int c) { return (r % VLOADS) * VBLK + (r / VLOADS) * ROWB + c; }
 };
 
 __device__ inline bf16x8_t zero_bf16x8() {
@@ -184,44 +224,21 @@ __device__ inline bf16x8_t zero_bf16x8() {
   return z;
 }
 
-// Queries of the current and of the pending step, 16 rows each (heads past G
-// are zero), and the pending step's M and 1/L per head (zero past G), staged
-// in LDS once per block and read per step, so they take no registers across
-// the loop.  Rows are padded by 16 bytes: the 16 lanes of a group read 16
-// different rows without bank conflicts.
-template <int D>
-struct QLds {
-  static constexpr int STRIDE = 2 * D + 16;
-  char q[2][16 * STRIDE];
-  float pm[16];
-  float pi[16];
-};
-
-// Fills one query tile from [G][D] bf16 in global memory.
+// A query group [G][D] (bf16, global memory) as the 16 x D MFMA operand,
+// heads past G zero: lane holds Q[head s][32 kk + 8 g4 .. +8].  Serves as B
+// of S^T = K Q^T and as A of S = Q K^T.
 template <int D, int G>
-__device__ inline void stage_q(char* tile, const void* src) {
-  constexpr int CPR = 2 * D / 16;  // 16-byte pieces per row
-  for (int i = threadIdx.x; i < 16 * CPR; i += kThreads) {
-    const int r = i / CPR, p = i % CPR;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (r < G) v = reinterpret_cast<const uint4*>(src)[r * CPR + p];
-    *reinterpret_cast<uint4*>(tile + r * QLds<D>::STRIDE + 16 * p) = v;
-  }
-}
-
-// MFMA operand of a staged query tile: lane holds Q[head s][32 kk + 8 g4 .. +8];
-// it serves as B of S^T = K Q^T and as A of S = Q K^T.
-template <int D>
-__device__ inline bf16x8_t q_operand(const char* tile, int s, int g4, int kk) {
-  return *reinterpret_cast<const bf16x8_t*>(tile + s * QLds<D>::STRIDE + 64 * kk + 16 * g4);
+__device__ inline bf16x8_t q_operand(const char* qgroup, int s, int g4, int kk) {
+  return (s < G) ? *reinterpret_cast<const bf16x8_t*>(qgroup + (long long)s * D * 2 + 64 * kk + 16 * g4)
+                 : zero_bf16x8();
 }
 
 template <int D, int G>
 __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pending<G>& pd, char* vtiles,
-                                QLds<D>& qs, CombineLds& cb) {
+                                CombineLds& cb) {
   using Cfg = MfmaCfg<D>;
-  constexpr int KK = Cfg::KK, NT = Cfg::NT, ROWB = Cfg::ROWB, VSTRIDE = Cfg::VSTRIDE;
-  constexpr int STEP = Cfg::STEP, LPR = Cfg::LPR, RPL = Cfg::RPL, VLOADS = Cfg::VLOADS;
+  constexpr int KK = Cfg::KK, NT = Cfg::NT, ROWB = Cfg::ROWB;
+  constexpr int STEP = Cfg::STEP, LPR = Cfg::LPR, VLOADS = Cfg::VLOADS;
   static_assert(G <= 8, "pending heads live in lane groups 0 and 1");
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -233,15 +250,23 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
 
   const int re = min(ck.r1, ck.ncache);
   const int pre_end = min(pd.rows, re);
-  stage_q<D, G>(qs.q[0], reinterpret_cast<const char*>(a.q) + ((long long)ck.b * HQ + (long long)ck.h * G) * D * 2);
-  if (pre_end > ck.r0) {
-    stage_q<D, G>(qs.q[1], pd.q);
-    if (tid < 16) {
-      qs.pm[tid] = tid < G ? pd.stat[tid] : 0.0f;
-      qs.pi[tid] = tid < G ? pd.stat[G + tid] : 0.0f;
-    }
+  // Both query sets live in registers; so do the pending step's statistics
+  // of the heads 4 g4 + rr this lane holds in S = Q_prev K^T.
+  const char* qcur = reinterpret_cast<const char*>(a.q) + ((long long)ck.b * HQ + (long long)ck.h * G) * D * 2;
+  bf16x8_t qb[KK], qo[KK];
+  float pm[4], pi[4];
+  const bool any_pending = pre_end > ck.r0;
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    qb[kk] = q_operand<D, G>(qcur, s, g4, kk);
+    qo[kk] = any_pending ? q_operand<D, G>(reinterpret_cast<const char*>(pd.q), s, g4, kk) : zero_bf16x8();
   }
-  __syncthreads();
+#pragma unroll
+  for (int rr = 0; rr < 4; ++rr) {
+    const int hh = 4 * g4 + rr;
+    pm[rr] = (any_pending && hh < G) ? pd.stat[hh] : 0.0f;
+    pi[rr] = (any_pending && hh < G) ? pd.stat[G + hh] : 0.0f;
+  }
 
   float m = kNegBig, l = 0.0f;
   f32x4_t o[NT];
@@ -261,11 +286,11 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
       for (int kk = 0; kk < KK; ++kk)
         kr[T][kk] = *reinterpret_cast<const bf16x8_t*>(Kb + (long long)row * ROWB + 64 * kk + 16 * g4);
     }
-    uint4 vr[VLOADS];
 #pragma unroll
     for (int u = 0; u < VLOADS; ++u) {
-      const int row = min(base + RPL * u + lane / LPR, re - 1);
-      vr[u] = *reinterpret_cast<const uint4*>(Vb + (long long)row * ROWB + 16 * (lane % LPR));
+      const int row = min(base + u + VLOADS * (lane / LPR), re - 1);
+      __builtin_amdgcn_global_load_lds((global_cvoid_t*)(Vb + (long long)row * ROWB + 16 * (lane % LPR)),
+                                       (lds_void_t*)((lds_char_t*)vb + u * Cfg::VBLK), 16, 0, 0);
     }
     // Pending update of this step's rows: lane groups 0 and 1 own rows
     // base + 16 g4 + s.
@@ -280,27 +305,20 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
     for (int T = 0; T < 2; ++T) {
       sacc[T] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        sacc[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], q_operand<D>(qs.q[0], s, g4, kk), sacc[T], 0, 0, 0);
+      for (int kk = 0; kk < KK; ++kk) sacc[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], qb[kk], sacc[T], 0, 0, 0);
     }
-#pragma unroll
-    for (int u = 0; u < VLOADS; ++u)
-      *reinterpret_cast<uint4*>(vb + (RPL * u + lane / LPR) * VSTRIDE + 16 * (lane % LPR)) = vr[u];
     if (pstep) {
       // S = Q_prev K^T: lane (g4, s) gets heads 4 g4 + rr of row 16 T + s.
-      const float4 pm = *reinterpret_cast<const float4*>(qs.pm + 4 * g4);
-      const float4 pi = *reinterpret_cast<const float4*>(qs.pi + 4 * g4);
       float part[2];
 #pragma unroll
       for (int T = 0; T < 2; ++T) {
         f32x4_t so = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
-          so = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q_operand<D>(qs.q[1], s, g4, kk), kr[T][kk], so, 0, 0, 0);
-        float acc = exp2f(fmaf(so[0], pd.scale, -pm.x)) * pi.x;
-        acc = fmaf(exp2f(fmaf(so[1], pd.scale, -pm.y)), pi.y, acc);
-        acc = fmaf(exp2f(fmaf(so[2], pd.scale, -pm.z)), pi.z, acc);
-        acc = fmaf(exp2f(fmaf(so[3], pd.scale, -pm.w)), pi.w, acc);
+          so = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qo[kk], kr[T][kk], so, 0, 0, 0);
+        float acc = 0.0f;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) acc = fmaf(exp2f(fmaf(so[rr], pd.scale, -pm[rr])), pi[rr], acc);
         part[T] = acc + __shfl_xor(acc, 16);
       }
       if (pon) pd.score[prow] = fmaf(pd.gamma, sold, g4 == 0 ? part[0] : part[1]);
@@ -343,9 +361,10 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int col = (16 * nt + 4 * (s & 3)) * 2;
-      const bf16x4_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(reinterpret_cast<lds_bf16x4_t*>(vbl + rsub * VSTRIDE + col));
+      const bf16x4_t a0 =
+          __builtin_amdgcn_ds_read_tr16_b64_v4bf16(reinterpret_cast<lds_bf16x4_t*>(vbl + Cfg::vaddr(rsub, col)));
       const bf16x4_t a1 =
-          __builtin_amdgcn_ds_read_tr16_b64_v4bf16(reinterpret_cast<lds_bf16x4_t*>(vbl + (rsub + 16) * VSTRIDE + col));
+          __builtin_amdgcn_ds_read_tr16_b64_v4bf16(reinterpret_cast<lds_bf16x4_t*>(vbl + Cfg::vaddr(rsub + 16, col)));
       const bf16x8_t av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
       o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ph, o[nt], 0, 0, 0);
       o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pl, o[nt], 0, 0, 0);
@@ -370,7 +389,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
     const uint32_t* kq = reinterpret_cast<const uint32_t*>(kn);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const bf16x8_t qv = q_operand<D>(qs.q[0], s, g4, kk);
+      const bf16x8_t qv = qb[kk];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bf16x2_t q2 = {qv[2 * j], qv[2 * j + 1]};
@@ -612,7 +631,6 @@ struct AttnLds<bf16_t, D> {
     char vtiles[kNumWaves * MfmaCfg<D>::TILE_BYTES];
     CombineLds cb;
   };
-  QLds<D> qs;
 };
 
 template <int D>
@@ -670,6 +688,29 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   ck.segrow0 = sbase + (long long)h * cp;
   const int ps = part_stride(G, D);
 
+  // Every block of the sequence counts itself once it has read len and the
+  // pending state (a release fence orders those reads before the count).  A
+  // block that finishes a segment later reads the count: all of them do so
+  // after every block of its segment has counted, so the last segment to
+  // finish sees the full count and publishes the new length and pending
+  // step; earlier finishers that also see it publish the same values.
+  const int pend_rows = a.pend_len[b];
+  const float pend_gamma = a.pend_gamma[b];
+  const float pend_scale = a.pend_scale[b];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  int32_t* seq_ctr = &a.seq_cnt[(long long)b * kCntStride];
+  if (tid == 0) __hip_atomic_fetch_add(seq_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int seq_full = a.HK * a.nch;
+  auto publish = [&](int seen) {
+    if (seen != seq_full) return;
+    if (app) a.len[b] = n_att;
+    a.pend_len[b] = n_att;
+    a.pend_par[b] = par ^ 1;
+    a.pend_gamma[b] = a.gamma;
+    a.pend_scale[b] = a.scale_log2;
+    __hip_atomic_store(seq_ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
+
   if (c == 0) {
     // Keep this step's queries of the group for the next call's score update.
     const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.q) + qgroup);
@@ -678,44 +719,40 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   }
   if (c < nne) {
     Pending<G> pd;
-    const int pl = a.pend_len[b];
-    pd.rows = pl > 0 ? min(pl, n) : 0;
+    pd.rows = pend_rows > 0 ? min(pend_rows, n) : 0;
     pd.score = a.score + ck.segrow0;
     pd.stat = a.segstat + (long long)seg * 2 * G;
     pd.q = reinterpret_cast<const char*>(a.qprev) + par * qhalf + qgroup;
-    pd.gamma = a.pend_gamma[b];
-    pd.scale = a.pend_scale[b];
+    pd.gamma = pend_gamma;
+    pd.scale = pend_scale;
     if constexpr (sizeof(T) == 2)
-      attn_chunk_mfma<D, G>(a, ck, pd, S.vtiles, S.qs, S.cb);
+      attn_chunk_mfma<D, G>(a, ck, pd, S.vtiles, S.cb);
     else
       attn_chunk_f32<D, G>(a, ck, pd, S.cb);
+    if (a.nch == 1) {
+      int seen = 0;
+      if (tid == 0) seen = __hip_atomic_load(seq_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      finish_single<D, G>(a, ck, S.cb);
+      if (tid == 0) publish(seen);
+      return;
+    }
     write_partial<D, G>(S.cb, a.part + ((long long)seg * a.nch + c) * ps);
   }
 
-  // Completion count: every block of the segment, with or without rows.
+  // Completion count of the segment: every block, with or without rows.
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (tid == 0)
     s_last = __hip_atomic_fetch_add(&a.seg_cnt[(long long)seg * kCntStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.nch - 1;
   __syncthreads();
   if (!s_last) return;
-
-  // Every block of this segment has read len and the pending state.
-  int seq_done = 0;
+  int seen = 0;
   if (tid == 0) {
     __hip_atomic_store(&a.seg_cnt[(long long)seg * kCntStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    seq_done = __hip_atomic_fetch_add(&a.seq_cnt[(long long)b * kCntStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.HK - 1;
+    seen = __hip_atomic_load(seq_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   combine_segment<D, G>(a, ck, nne);
-  if (seq_done) {
-    // ... and so has every block of the sequence.
-    if (app) a.len[b] = n_att;
-    a.pend_len[b] = n_att;
-    a.pend_par[b] = par ^ 1;
-    a.pend_gamma[b] = a.gamma;
-    a.pend_scale[b] = a.scale_log2;
-    __hip_atomic_store(&a.seq_cnt[(long long)b * kCntStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  if (tid == 0) publish(seen);
 }
 
 // bf16: three resident blocks per CU need at most 168 registers per lane.
