@@ -838,8 +838,8 @@ __global__ void flush_clear_kernel(int32_t* pend_len, int count) {
   if (i < count) pend_len[i] = 0;
 }
 
-// Optional tuning overrides, read once: LETHE_DECODE_BLOCKS (blocks to aim
-// for per launch) and LETHE_DECODE_MIN_CHUNK (rows).
+// Optional tuning overrides, read at every call: LETHE_DECODE_BLOCKS (blocks
+// to aim for per launch) and LETHE_DECODE_MIN_CHUNK (rows).
 int env_int(const char* name) {
   const char* v = getenv(name);
   return v ? atoi(v) : 0;
@@ -851,8 +851,8 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   // Resident blocks per device for this instantiation; the value depends only
   // on the device, so concurrent first calls store the same number.
   static int resident[64];
-  static const int env_blocks = env_int("LETHE_DECODE_BLOCKS");
-  static const int env_chunk = env_int("LETHE_DECODE_MIN_CHUNK");
+  const int env_blocks = env_int("LETHE_DECODE_BLOCKS");
+  const int env_chunk = env_int("LETHE_DECODE_MIN_CHUNK");
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return LETHE_ERR_HIP;
   int blocks = (dev >= 0 && dev < 64) ? __atomic_load_n(&resident[dev], __ATOMIC_RELAXED) : 0;

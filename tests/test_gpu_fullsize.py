@@ -1,0 +1,179 @@
+"""GPU parity at the benchmark workloads' full per-layer sizes (run on an MI355X).
+
+For each of the Llama-8B / Qwen-7B workloads (batch, KV heads, head_dim and
+the full cached lengths of one layer: 2k, 16k, U[8k, 32k], logU[1k, 64k]) a
+two-layer cache is filled by the seeded Zipf generator and driven through
+the library with its default launch configuration (the one bench.py times):
+two decode steps with append, then a prune round.  The oracle recomputes a
+sample of segments one by one (the shortest and longest sequences and a few
+seeded picks):
+
+* attention outputs and scores within |gpu - ref| <= 1e-3 + 2e-3 |ref|;
+* layer sparsity within 1e-6 of the oracle's Hoyer value of the same scores;
+* budgets bit-exact for every sequence given the device's sparsities;
+* keep masks and compacted K / V / score rows bit-exact given the device's
+  scores.
+
+Configs with 512 or more segments per layer run one chunk per segment; the
+others split segments across blocks, so both decode paths are covered.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2511_06029_amd import lethe as L
+from workloads import CONFIGS
+from workloads.synth import ZipfCache
+
+pytestmark = pytest.mark.gpu
+
+ATOL, RTOL = 1e-3, 2e-3
+DEV = "cuda"
+LAYERS = 2
+STEPS = 2
+
+
+def note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def close(gpu, ref, what):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    bad = ~(np.abs(gpu - ref) <= ATOL + RTOL * np.abs(ref))
+    if bad.any():
+        i = np.flatnonzero(bad.ravel())[0]
+        raise AssertionError("%s: %d mismatches, first at %d: gpu %r ref %r" %
+                             (what, bad.sum(), i, gpu.ravel()[i], ref.ravel()[i]))
+
+
+def f32(t):
+    return t.detach().float().cpu().numpy()
+
+
+def sample_seqs(lengths, k=6, seed=0):
+    order = np.argsort(lengths, kind="stable")
+    rng = np.random.default_rng(seed)
+    picks = {int(order[0]), int(order[-1])}
+    for b in rng.permutation(len(lengths)):
+        if len(picks) >= k:
+            break
+        picks.add(int(b))
+    return sorted(picks)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("cfg_id", [2, 3, 4, 5])
+def test_fullsize_decode_and_prune(cfg_id):
+    cfg = CONFIGS[cfg_id]
+    gen = ZipfCache(cfg_id, device=DEV)
+    T = gen.lengths()
+    B, HQ, HK, D, G = cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.group
+    caps = [int(t) + STEPS for t in T]
+    note("fullsize config %d: B=%d HK=%d G=%d lengths %d..%d, %d layers" % (cfg_id, B, HK, G, T.min(), T.max(), LAYERS))
+    c = L.LetheCache(LAYERS, caps, HQ, HK, D, dtype="bf16", device=DEV)
+    for l in range(LAYERS):
+        for b in range(B):
+            K, V = gen.segment(l, b, int(T[b]), T=int(T[b]))
+            for h in range(HK):
+                s0, _ = c.seg_rows(b, h)
+                c.k[l, s0:s0 + int(T[b])] = K[h]
+                c.v[l, s0:s0 + int(T[b])] = V[h]
+            del K, V
+    c.len.copy_(torch.from_numpy(np.tile(T.astype(np.int32), (LAYERS, 1))).to(DEV))
+    ws = c.workspace(L.OP_DECODE)
+    torch.cuda.synchronize()
+
+    picks = sample_seqs(T)
+    # Oracle state of the sampled segments: K, V as stored (bf16 values), s in fp64.
+    ref = {}
+    for l in range(LAYERS):
+        for b in picks:
+            for h in range(HK):
+                s0, _ = c.seg_rows(b, h)
+                n = int(T[b])
+                ref[l, b, h] = [f32(c.k[l, s0:s0 + n]), f32(c.v[l, s0:s0 + n]), np.zeros(n)]
+    scale = 1.0 / math.sqrt(D)
+    for t in range(STEPS):
+        note("fullsize config %d: decode step %d" % (cfg_id, t))
+        for l in range(LAYERS):
+            q, kn, vn = gen.step(t, l, T=T + t)
+            out = torch.empty((B, HQ, D), dtype=torch.float32, device=DEV)
+            L.decode_attn_score(c, l, q, kn, vn, cfg.gamma, 0.0, out, ws)
+            torch.cuda.synchronize()
+            og, qh, kh, vh = f32(out), f32(q), f32(kn), f32(vn)
+            for b in picks:
+                for h in range(HK):
+                    K, V, s = ref[l, b, h]
+                    K = np.vstack([K, kh[b, h][None]])
+                    V = np.vstack([V, vh[b, h][None]])
+                    s = np.append(s, 0.0)
+                    o, s = oracle.attend(qh[b, h * G:(h + 1) * G], K, V, s, cfg.gamma, scale)
+                    ref[l, b, h] = [K, V, s]
+                    close(og[b, h * G:(h + 1) * G], o, "cfg%d out step %d l%d b%d h%d" % (cfg_id, t, l, b, h))
+    assert int(c.dev_status[0]) == 0
+    assert (c.len.cpu().numpy() == (T + STEPS).astype(np.int32)[None]).all()
+    c.flush()
+    torch.cuda.synchronize()
+    for (l, b, h), (K, V, s) in ref.items():
+        s0, _ = c.seg_rows(b, h)
+        close(f32(c.score[l, s0:s0 + K.shape[0]]), s, "cfg%d scores l%d b%d h%d" % (cfg_id, l, b, h))
+
+    note("fullsize config %d: prune round" % cfg_id)
+    n_now = (T + STEPS).astype(np.int64)
+    gbud = torch.from_numpy((np.floor(cfg.budget_frac * n_now).astype(np.int64)) * LAYERS).to(DEV)
+    S = torch.empty((B, LAYERS), dtype=torch.float32, device=DEV)
+    bud = torch.empty((B, LAYERS), dtype=torch.int32, device=DEV)
+    L.layer_sparsity(c, gbud, cfg.recent, cfg.sink, None, S, bud)
+    torch.cuda.synchronize()
+    Sh = S.cpu().numpy()
+    for b in picks:
+        for l in range(LAYERS):
+            n = int(n_now[b])
+            a = np.zeros(n)
+            for h in range(HK):
+                s0, _ = c.seg_rows(b, h)
+                a += c.score[l, s0:s0 + n].double().cpu().numpy()
+            assert abs(float(Sh[b, l]) - oracle.hoyer(a)) <= 1e-6, (cfg_id, b, l)
+    # Budgets: bit-exact for every sequence given the device's sparsities.
+    L.layer_sparsity(c, gbud, cfg.recent, cfg.sink, S, S, bud)
+    torch.cuda.synchronize()
+    bh = bud.cpu().numpy()
+    gb = gbud.cpu().numpy()
+    for b in range(B):
+        want, _ = oracle.budget_split(np.full(LAYERS, n_now[b], np.int32), Sh[b], cfg.recent, cfg.sink, gb[b])
+        np.testing.assert_array_equal(bh[b], want, err_msg="cfg%d budgets b%d" % (cfg_id, b))
+    keep = torch.zeros((LAYERS, c.rows_per_layer), dtype=torch.uint8, device=DEV)
+    L.rasr_select(c, bud, cfg.recent, cfg.sink, keep)
+    torch.cuda.synchronize()
+    before = {}
+    for l in range(LAYERS):
+        for b in picks:
+            for h in range(HK):
+                s0, _ = c.seg_rows(b, h)
+                n = int(n_now[b])
+                sc = c.score[l, s0:s0 + n].cpu().numpy()
+                km = keep[l, s0:s0 + n].cpu().numpy().astype(bool)
+                want = oracle.rasr_select(sc, int(bh[b, l]), cfg.recent, cfg.sink)
+                np.testing.assert_array_equal(km, want, err_msg="cfg%d keep l%d b%d h%d" % (cfg_id, l, b, h))
+                before[l, b, h] = (c.k[l, s0:s0 + n].view(torch.int16).cpu().numpy(),
+                                   c.v[l, s0:s0 + n].view(torch.int16).cpu().numpy(), sc, km)
+    L.kv_compact(c, keep, c.workspace(L.OP_COMPACT))
+    torch.cuda.synchronize()
+    assert int(c.dev_status[0]) == 0
+    lens = c.len.cpu().numpy()
+    for (l, b, h), (kb, vb, sb, km) in before.items():
+        s0, _ = c.seg_rows(b, h)
+        m = int(km.sum())
+        assert lens[l, b] == m == min(int(n_now[b]), int(bh[b, l]))
+        np.testing.assert_array_equal(c.k[l, s0:s0 + m].view(torch.int16).cpu().numpy(), oracle.compact(kb, km))
+        np.testing.assert_array_equal(c.v[l, s0:s0 + m].view(torch.int16).cpu().numpy(), oracle.compact(vb, km))
+        np.testing.assert_array_equal(c.score[l, s0:s0 + m].cpu().numpy().view(np.uint32),
+                                      oracle.compact(sb, km).view(np.uint32))
+    del c, ws
+    torch.cuda.empty_cache()
