@@ -277,28 +277,43 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
   const char* Vb = reinterpret_cast<const char*>(a.v) + ck.segrow0 * ROWB;
   const float sc = a.scale_log2;
 
-  for (int base = ck.r0 + STEP * w; base < re; base += STEP * kNumWaves) {
-    bf16x8_t kr[2][KK];
+  // Loads of a step: K rows into the operand registers and, for the pending
+  // update, the old scores of rows base + 16 g4 + s (lane groups 0 and 1);
+  // V rows straight into the wave's LDS tile.  The next step's K and scores
+  // are requested as soon as this step's K has gone through the MFMAs, and
+  // its V as soon as this step's V^T reads have completed, so the loads of
+  // one step overlap the softmax and PV work of the previous one.
+  bf16x8_t kr[2][KK];
+  float sold = 0.0f;
+  auto load_k = [&](int bs) {
 #pragma unroll
     for (int T = 0; T < 2; ++T) {
-      const int row = min(base + 16 * T + s, re - 1);
+      const int row = min(bs + 16 * T + s, re - 1);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
         kr[T][kk] = *reinterpret_cast<const bf16x8_t*>(Kb + (long long)row * ROWB + 64 * kk + 16 * g4);
     }
+    const int prow = bs + 16 * g4 + s;
+    sold = (g4 < 2 && prow < pre_end) ? pd.score[prow] : 0.0f;
+  };
+  auto load_v = [&](int bs) {
 #pragma unroll
     for (int u = 0; u < VLOADS; ++u) {
-      const int row = min(base + u + VLOADS * (lane / LPR), re - 1);
+      const int row = min(bs + u + VLOADS * (lane / LPR), re - 1);
       __builtin_amdgcn_global_load_lds((global_cvoid_t*)(Vb + (long long)row * ROWB + 16 * (lane % LPR)),
                                        (lds_void_t*)((lds_char_t*)vb + u * Cfg::VBLK), 16, 0, 0);
     }
-    // Pending update of this step's rows: lane groups 0 and 1 own rows
-    // base + 16 g4 + s.
+  };
+  const int wstride = STEP * kNumWaves;
+  if (ck.r0 + STEP * w < re) {
+    load_k(ck.r0 + STEP * w);
+    load_v(ck.r0 + STEP * w);
+  }
+  for (int base = ck.r0 + STEP * w; base < re; base += wstride) {
+    const bool more = base + wstride < re;  // wave-uniform
     const bool pstep = base < pre_end;
     const int prow = base + 16 * g4 + s;
     const bool pon = pstep && g4 < 2 && prow < pre_end;
-    float sold = 0.0f;
-    if (pon) sold = pd.score[prow];
 
     f32x4_t sacc[2];
 #pragma unroll
@@ -323,6 +338,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
       }
       if (pon) pd.score[prow] = fmaf(pd.gamma, sold, g4 == 0 ? part[0] : part[1]);
     }
+    if (more) load_k(base + wstride);
 
     // Logits of rows base + 16 T + 4 g4 + rr for head s.
     float x[2][4];
@@ -369,6 +385,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
       o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ph, o[nt], 0, 0, 0);
       o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pl, o[nt], 0, 0, 0);
     }
+    if (more) load_v(base + wstride);
   }
 
   // The appended row (last chunk of its segment), by wave 0: read from
