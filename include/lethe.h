@@ -150,6 +150,10 @@ size_t lethe_state_bytes(const lethe_cache* cache);
  *  out     fp32 [num_seqs][num_q_heads][head_dim]
  *  ws      at least lethe_workspace_bytes(cache, LETHE_OP_DECODE) bytes.
  * A sequence skipped for overflow or a bad layout keeps its pending step.
+ * The rows of a segment are shared among blocks at run time, so repeated calls
+ * on identical inputs can differ in the last bits of out and score; with the
+ * environment variable LETHE_DECODE_DETERMINISTIC set to a non-zero value the
+ * split is fixed and repeated calls are bit-identical.
  * Accumulation is fp32; results match the exact result to about 1e-5
  * relative.  Errors: LETHE_ERR_INVALID (null pointer, layer out of range,
  * gamma outside (0, 1] or NaN, NaN scale), LETHE_ERR_UNSUPPORTED,

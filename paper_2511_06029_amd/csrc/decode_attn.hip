@@ -1,35 +1,39 @@
 // Decode attention fused with the RASR importance update (Eq. 5), gfx950.
 //
-// One launch handles one layer for every sequence.  The live rows of each
-// (sequence, KV head) segment are cut into at most `nch` chunks of a multiple
-// of 32 rows (split-K flash decoding); block (segment, c) owns chunk c, so the
-// mapping needs no plan and no length ever travels to the host.  Blocks past
-// a segment's last chunk only take part in its completion count.
+// One launch handles one layer for every sequence.  Each (sequence, KV head)
+// segment gets nch blocks (split-K flash decoding), spread over the grid
+// (block i serves segment i mod segments).  The cached rows of a segment are
+// cut into 32-row steps that the segment's wavefronts take from a per-segment
+// counter, so a block that the memory system serves faster simply takes more
+// steps; no plan kernel and no length on the host.
 //
-// Per block (4 wavefronts):
-//  - bf16 storage: each wavefront walks 32-row steps.  S^T = K Q^T runs on
-//    the matrix cores (v_mfma_f32_16x16x32_bf16: 16 rows x the group's G query
-//    heads padded to 16; K rows load straight into the operand layout).  The
-//    softmax is online and in base 2, one head per lane.  O^T = V^T P^T: the
-//    step's V rows are staged in the wavefront's own LDS tile and read back
-//    transposed (ds_read_b64_tr_b16); P is split into bf16 high and low parts
-//    (two MFMAs) so the products keep fp32-level accuracy.  fp32 storage takes
-//    a VALU path with the same outputs.
-//  - Eq. 5 runs one call late: the score update of a step needs the step's
-//    final max and sum per head, known only once every chunk is done.  The
-//    call keeps its query, scale and per-head (M, 1/L); the next call on the
-//    layer recomputes that step's logits from the K rows it loads anyway (one
-//    more MFMA chain, Q_prev K^T) and applies
-//        s <- gamma s + sum_g exp2(x_g - M_g) / L_g
-//    to those rows.  launch_flush applies a pending step on its own.
-//  - Every block bumps its sequence's counter once it has read len and the
-//    pending state; the last one publishes the new length and pending step
-//    (nobody of this launch reads them afterwards).
-//  - With one chunk per segment the block writes out and the step's (M, 1/L)
-//    per head itself.  Otherwise the chunk's (m, l, o) partial goes to the
-//    workspace with write-through stores, then the block bumps its segment's
-//    counter; the last block of a segment combines the partials.  Counters go
-//    back to zero.
+// Per wavefront and step (bf16 storage):
+//  - S^T = K Q^T on the matrix cores (v_mfma_f32_16x16x32_bf16: 16 rows x
+//    the group's G query heads padded to 16; K rows load straight into the
+//    operand layout).  Online softmax in base 2, one head per lane.
+//  - O^T = V^T P^T: the step's V rows reach the wavefront's LDS tile by
+//    direct loads and are read back transposed (ds_read_b64_tr_b16); P is
+//    split into bf16 high and low parts (two MFMAs) so the products keep
+//    fp32-level accuracy.
+//  - The next step's K rows are requested as soon as this step's K has gone
+//    through the MFMAs, its V once this step's V^T reads have completed.
+// fp32 storage takes a VALU path with the same outputs.
+//
+// Eq. 5 runs one call late: the score update of a step needs the step's final
+// max and sum per head, known only once every block is done.  The call keeps
+// its query, scale and per-head (M, 1/L); the next call on the layer
+// recomputes that step's logits from the K rows it loads anyway (one more
+// MFMA chain, Q_prev K^T) and applies s <- gamma s + sum_g exp2(x_g - M_g) / L_g
+// to those rows.  launch_flush applies a pending step on its own.
+//
+// Every block bumps its sequence's counter once it has read len and the
+// pending state; the block that finishes a segment publishes the new length
+// and pending step when the count is full (nobody of this launch reads them
+// afterwards).  With one block per segment the block writes out and the
+// step's (M, 1/L) itself.  Otherwise each block's (m, l, o) partial goes to
+// the workspace with write-through stores, then the block bumps its segment's
+// counter; the last block of a segment combines the partials.  Counters go
+// back to zero.
 #include <math.h>
 #include <stdlib.h>
 
@@ -68,11 +72,28 @@ __device__ inline float2 ld_agent2(const float* p) {
 // What one block works on.
 struct Chunk {
   int b, h, seg, c;
-  int r0, r1;        // rows [r0, r1) of the segment (r1 - 1 may be the appended row)
   int ncache;        // rows already in the cache; the appended row is row ncache
   bool app;          // a row is appended to this sequence
   long long segrow0; // first row of the segment in the layer
+  int32_t* next;     // the segment's step counter
+  int first, stride; // fixed schedule: steps first, first + stride, ... (stride 0: counter)
 };
+
+// A wavefront's next step: from the segment's counter (whichever wave asks
+// first), or from the fixed schedule.  step_request issues the request (the
+// counter's reply lands in lane 0 of the returned register); step_index reads
+// it when it is needed, so the atomic's latency overlaps other work.
+__device__ inline int step_request(const Chunk& ck, int& fixed_next, int lane) {
+  if (ck.stride) {
+    const int v = fixed_next;
+    fixed_next += ck.stride;
+    return v;
+  }
+  int v = 0;
+  if (lane == 0) v = __hip_atomic_fetch_add(ck.next, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return v;
+}
+__device__ inline int step_index(int raw) { return __builtin_amdgcn_readfirstlane(raw); }
 
 // The pending step of a segment: rows [0, rows) get
 //   s <- gamma s + sum_g exp2(scale * q_g . k - M_g) * invL_g
@@ -248,14 +269,15 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
   const int HQ = a.HK * G;
   char* vb = vtiles + w * Cfg::TILE_BYTES;
 
-  const int re = min(ck.r1, ck.ncache);
+  const int re = ck.ncache;
   const int pre_end = min(pd.rows, re);
+  const int nsteps = (re + STEP - 1) / STEP;
   // Both query sets live in registers; so do the pending step's statistics
   // of the heads 4 g4 + rr this lane holds in S = Q_prev K^T.
   const char* qcur = reinterpret_cast<const char*>(a.q) + ((long long)ck.b * HQ + (long long)ck.h * G) * D * 2;
   bf16x8_t qb[KK], qo[KK];
   float pm[4], pi[4];
-  const bool any_pending = pre_end > ck.r0;
+  const bool any_pending = pre_end > 0;
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     qb[kk] = q_operand<D, G>(qcur, s, g4, kk);
@@ -304,13 +326,19 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
                                        (lds_void_t*)((lds_char_t*)vb + u * Cfg::VBLK), 16, 0, 0);
     }
   };
-  const int wstride = STEP * kNumWaves;
-  if (ck.r0 + STEP * w < re) {
-    load_k(ck.r0 + STEP * w);
-    load_v(ck.r0 + STEP * w);
+  int fixed_next = ck.first + w;
+  int graw = step_request(ck, fixed_next, lane);
+  int idx = step_index(graw);
+  int nidx = nsteps + 1;
+  if (idx < nsteps) {
+    load_k(idx * STEP);
+    load_v(idx * STEP);
+    graw = step_request(ck, fixed_next, lane);
   }
-  for (int base = ck.r0 + STEP * w; base < re; base += wstride) {
-    const bool more = base + wstride < re;  // wave-uniform
+  while (idx < nsteps) {
+    const int base = idx * STEP;
+    nidx = step_index(graw);
+    const bool more = nidx < nsteps;  // wave-uniform
     const bool pstep = base < pre_end;
     const int prow = base + 16 * g4 + s;
     const bool pon = pstep && g4 < 2 && prow < pre_end;
@@ -338,7 +366,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
       }
       if (pon) pd.score[prow] = fmaf(pd.gamma, sold, g4 == 0 ? part[0] : part[1]);
     }
-    if (more) load_k(base + wstride);
+    if (more) load_k(nidx * STEP);
 
     // Logits of rows base + 16 T + 4 g4 + rr for head s.
     float x[2][4];
@@ -385,13 +413,17 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
       o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ph, o[nt], 0, 0, 0);
       o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pl, o[nt], 0, 0, 0);
     }
-    if (more) load_v(base + wstride);
+    if (more) {
+      load_v(nidx * STEP);
+      graw = step_request(ck, fixed_next, lane);
+    }
+    idx = nidx;
   }
 
   // The appended row (last chunk of its segment), by wave 0: read from
   // k_new / v_new, copied into the cache, its score started at 0, and folded
   // into wave 0's state.
-  if (ck.app && ck.r1 == ck.ncache + 1 && w == 0) {
+  if (ck.app && idx == nsteps) {
     const char* kn = reinterpret_cast<const char*>(a.k_new) + (((long long)ck.b * a.HK + ck.h) * D) * 2;
     const char* vn = reinterpret_cast<const char*>(a.v_new) + (((long long)ck.b * a.HK + ck.h) * D) * 2;
     if (lane < LPR) {
@@ -459,7 +491,6 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
   constexpr int RPW = kWave / LPR;
   constexpr int U = 4;
   constexpr int ROWS_WAVE = U * RPW;
-  constexpr int ROWS_BLOCK = ROWS_WAVE * kNumWaves;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int w = tid / kWave;
@@ -481,8 +512,9 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
       qf[g][3] = __uint_as_float(r.w) * a.scale_log2;
     }
   }
-  const int re = min(ck.r1, ck.ncache);
+  const int re = ck.ncache;
   const int pre_end = min(pd.rows, re);
+  const int nsteps = (re + ROWS_WAVE - 1) / ROWS_WAVE;
   float pM[G], pI[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -491,7 +523,7 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
 #pragma unroll
     for (int e = 0; e < EPL; ++e) qof[g][e] = 0.0f;
   }
-  if (pre_end > ck.r0) {
+  if (pre_end > 0) {
     const float* qp = reinterpret_cast<const float*>(pd.q) + dp * EPL;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -566,7 +598,11 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
     }
   };
 
-  for (int base = ck.r0 + w * ROWS_WAVE; base < re; base += ROWS_BLOCK) {
+  int fixed_next = ck.first + w;
+  auto grab = [&]() { return step_index(step_request(ck, fixed_next, lane)); };
+  int idx = grab();
+  for (; idx < nsteps; idx = grab()) {
+    const int base = idx * ROWS_WAVE;
     uint4 kr[U], vr[U];
     int row[U];
     bool valid[U];
@@ -583,7 +619,7 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
     }
     consume(kr, vr, valid, pstep, row, sold);
   }
-  if (ck.app && ck.r1 == ck.ncache + 1 && w == 0) {
+  if (ck.app && idx == nsteps) {
     const long long nb = ((long long)ck.b * a.HK + ck.h) * D + dp * EPL;
     uint4 kr[U], vr[U];
     int row[U];
@@ -660,8 +696,11 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   __shared__ __attribute__((aligned(16))) AttnLds<T, D> S;
   __shared__ int s_last;
   const int tid = threadIdx.x;
-  const int seg = blockIdx.x / a.nch;
-  const int c = blockIdx.x - seg * a.nch;
+  // Block c of segment seg: the nch blocks of a segment are spread over the
+  // grid (and over the dispatch order).
+  const int segs = a.B * a.HK;
+  const int seg = (int)(blockIdx.x % segs);
+  const int c = (int)(blockIdx.x / segs);
   const int b = seg / a.HK;
   const int h = seg - b * a.HK;
   const int HQ = a.HK * G;
@@ -685,10 +724,6 @@ __device__ inline void decode_body(const DecodeArgs& a) {
     }
     return;
   }
-  int csz = (n_att + a.nch - 1) / a.nch;
-  csz = ((csz + 31) / 32) * 32;
-  if (csz < a.min_chunk) csz = a.min_chunk;
-  const int nne = (n_att + csz - 1) / csz;  // chunks with rows
   const int par = a.pend_par[b] & 1;
   const size_t qgroup = ((size_t)b * HQ + (size_t)h * G) * D * sizeof(T);  // bytes
   const size_t qhalf = (size_t)a.B * HQ * D * sizeof(T);
@@ -698,8 +733,9 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   ck.h = h;
   ck.seg = seg;
   ck.c = c;
-  ck.r0 = c * csz;
-  ck.r1 = min(ck.r0 + csz, n_att);
+  ck.next = &a.seg_cnt[(long long)seg * kCntStride + kStepCounter];
+  ck.first = c * kNumWaves;  // fixed schedule: wave w starts at step c * waves + w
+  ck.stride = a.deterministic ? a.nch * kNumWaves : 0;
   ck.app = app;
   ck.ncache = n;
   ck.segrow0 = sbase + (long long)h * cp;
@@ -734,7 +770,7 @@ __device__ inline void decode_body(const DecodeArgs& a) {
     uint4* dst = reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.qprev) + (par ^ 1) * qhalf + qgroup);
     for (int i = tid; i < (int)(G * D * sizeof(T) / 16); i += kThreads) dst[i] = src[i];
   }
-  if (c < nne) {
+  {
     Pending<G> pd;
     pd.rows = pend_rows > 0 ? min(pend_rows, n) : 0;
     pd.score = a.score + ck.segrow0;
@@ -750,13 +786,16 @@ __device__ inline void decode_body(const DecodeArgs& a) {
       int seen = 0;
       if (tid == 0) seen = __hip_atomic_load(seq_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       finish_single<D, G>(a, ck, S.cb);
-      if (tid == 0) publish(seen);
+      if (tid == 0) {
+        publish(seen);
+        __hip_atomic_store(ck.next, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
       return;
     }
     write_partial<D, G>(S.cb, a.part + ((long long)seg * a.nch + c) * ps);
   }
 
-  // Completion count of the segment: every block, with or without rows.
+  // Completion count of the segment: every block, with or without steps.
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (tid == 0)
@@ -766,9 +805,10 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   int seen = 0;
   if (tid == 0) {
     __hip_atomic_store(&a.seg_cnt[(long long)seg * kCntStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(ck.next, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     seen = __hip_atomic_load(seq_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  combine_segment<D, G>(a, ck, nne);
+  combine_segment<D, G>(a, ck, a.nch);
   if (tid == 0) publish(seen);
 }
 
@@ -855,8 +895,9 @@ __global__ void flush_clear_kernel(int32_t* pend_len, int count) {
   if (i < count) pend_len[i] = 0;
 }
 
-// Optional tuning overrides, read at every call: LETHE_DECODE_BLOCKS (blocks
-// to aim for per launch) and LETHE_DECODE_MIN_CHUNK (rows).
+// Overrides read at every call: LETHE_DECODE_BLOCKS (blocks to aim for per
+// launch; default two per CU) and LETHE_DECODE_DETERMINISTIC (non-zero: fixed
+// step schedule, so repeated calls give bit-identical results).
 int env_int(const char* name) {
   const char* v = getenv(name);
   return v ? atoi(v) : 0;
@@ -869,7 +910,6 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   // on the device, so concurrent first calls store the same number.
   static int resident[64];
   const int env_blocks = env_int("LETHE_DECODE_BLOCKS");
-  const int env_chunk = env_int("LETHE_DECODE_MIN_CHUNK");
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return LETHE_ERR_HIP;
   int blocks = (dev >= 0 && dev < 64) ? __atomic_load_n(&resident[dev], __ATOMIC_RELAXED) : 0;
@@ -881,7 +921,13 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
     blocks = cus * (per_cu < 1 ? 1 : per_cu);
     if (dev >= 0 && dev < 64) __atomic_store_n(&resident[dev], blocks, __ATOMIC_RELAXED);
   }
-  const int target = env_blocks > 0 ? env_blocks : blocks;
+  int target = env_blocks;
+  if (target <= 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return LETHE_ERR_HIP;
+    target = blocks < 2 * cus ? blocks : 2 * cus;
+  }
+  a.deterministic = env_int("LETHE_DECODE_DETERMINISTIC") != 0;
   const int64_t segs = (int64_t)a.B * a.HK;
   int64_t nch = target / segs;
   const int64_t cap_nch = decode_max_chunks(a.B, a.HK) / segs;
@@ -889,7 +935,6 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   if (nch > kMaxChunksPerSeg) nch = kMaxChunksPerSeg;
   if (nch < 1) nch = 1;
   a.nch = (int32_t)nch;
-  a.min_chunk = env_chunk > 0 ? ((env_chunk + 31) / 32) * 32 : 128;
   const auto kernel = decode_kernel<T, D, G>();
   hipLaunchKernelGGL(kernel, dim3((unsigned)(segs * nch)), dim3(kThreads), 0, s, a);
   if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;

@@ -158,7 +158,7 @@ lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const 
   a.part = (float*)ws;
   a.dev_status = c->dev_status;
   a.nch = 0;  // chosen by the launcher
-  a.min_chunk = 0;
+  a.deterministic = 0;
   return launch_decode(a, c->dtype, D, G, stream);
 }
 

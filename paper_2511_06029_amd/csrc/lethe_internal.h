@@ -34,13 +34,17 @@ __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a -
 //   pend_par   [L][B]               which half of qprev holds the pending query
 //   pend_gamma [L][B]               decay of the pending step
 //   pend_scale [L][B]               softmax scale * log2(e) of the pending step
-//   seg_cnt    [B*HK] x kCntStride  blocks of a segment done (0 between calls)
+//   seg_cnt    [B*HK] x kCntStride  blocks of a segment done, and the
+//                                   segment's next step (0 between calls)
 //   seq_cnt    [B] x kCntStride     segments of a sequence done (0 between calls)
 //   segstat    [L][B*HK][2G]        per head: M (max scaled logit), then 1 / L
 //   qprev      [L][2][B][HQ][D]     queries (storage type), double buffered
 // Counters sit kCntStride words apart so the atomics of different segments
-// meet in different cache lines and memory channels.
+// meet in different cache lines and memory channels.  A segment's slot also
+// holds, kStepCounter words in, the counter its wavefronts take decode steps
+// from.
 constexpr int kCntStride = 64;
+constexpr int kStepCounter = 32;
 
 struct StateLayout {
   size_t len_off, par_off, gamma_off, scale_off, seg_cnt_off, seq_cnt_off, stat_off, q_off, total;
@@ -105,8 +109,8 @@ struct DecodeArgs {
   int32_t* seq_cnt;      // [B] x kCntStride
   float* part;           // workspace
   int32_t* dev_status;
-  int32_t nch;           // chunks per segment, 1 .. kMaxChunksPerSeg
-  int32_t min_chunk;     // rows, multiple of 32
+  int32_t nch;           // blocks per segment, 1 .. kMaxChunksPerSeg
+  int32_t deterministic; // fixed step schedule instead of the step counter
 };
 
 struct FlushArgs {

@@ -206,19 +206,22 @@ def test_decode_matches_oracle(dtype, D, G, HK, lengths, append):
     assert int(H.c.dev_status[0]) == 0
 
 
-@pytest.mark.parametrize("env", [{"LETHE_DECODE_BLOCKS": "1"},
-                                 {"LETHE_DECODE_BLOCKS": "8192", "LETHE_DECODE_MIN_CHUNK": "32"}])
+@pytest.mark.parametrize("env", [{"LETHE_DECODE_BLOCKS": "1"}, {"LETHE_DECODE_BLOCKS": "8192"},
+                                 {"LETHE_DECODE_DETERMINISTIC": "1"},
+                                 {"LETHE_DECODE_BLOCKS": "8192", "LETHE_DECODE_DETERMINISTIC": "1"}])
 @pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[3], SHAPES[5], SHAPES[7]])
 def test_decode_chunking_extremes(env, shape, monkeypatch):
-    """One chunk per segment (the block writes its output itself) and 32-row
-    chunks with up to 64 blocks per segment, many of them empty."""
+    """One block per segment (the block writes its output itself) and up to 64
+    blocks per segment, many of which find no step left."""
     for k, v in env.items():
         monkeypatch.setenv(k, v)
     test_decode_matches_oracle(*shape)
 
 
-def test_decode_deterministic_and_empty():
+def test_decode_deterministic_and_empty(monkeypatch):
+    """With the fixed step schedule repeated calls are bit-identical."""
     note("decode determinism")
+    monkeypatch.setenv("LETHE_DECODE_DETERMINISTIC", "1")
     rng = np.random.default_rng(7)
     lengths = [1000, 0, 3000]
     H = Harness(1, [4000] * 3, 32, 8, 128, "bf16")
