@@ -3,7 +3,8 @@
 Plain, slow CPU reference for the Lethe hot path (arXiv 2511.06029): decode
 attention with importance accumulation (Eq. 5), per-layer Hoyer sparsity
 (Eq. 1 on the head-summed score of Eq. 2), the layer budget split, RASR
-retention and order-preserving compaction.
+retention (per KV head, or shared by the heads of a layer), Algorithm 1's
+segmented shrinking with its size trigger, and order-preserving compaction.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  It shares no code with the HIP path and
@@ -39,6 +40,10 @@ def _load():
         lib.lethe_oracle_budget.restype = ctypes.c_int
         lib.lethe_oracle_select.argtypes = [i64, vp, i64, i32, i32, vp]
         lib.lethe_oracle_select.restype = ctypes.c_int
+        lib.lethe_oracle_head_sum_f32.argtypes = [i64, ctypes.c_int, vp, vp]
+        lib.lethe_oracle_head_sum_f32.restype = None
+        lib.lethe_oracle_shrink.argtypes = [i64, vp, i32, ctypes.c_float, i32, i32, vp, vp]
+        lib.lethe_oracle_shrink.restype = i64
         _lib = lib
     return _lib
 
@@ -110,6 +115,43 @@ def rasr_select(s, k, recent, sink):
     if rc != 0:
         raise MemoryError("oracle select failed")
     return keep[:n].astype(bool)
+
+
+def head_sum_f32(s_heads):
+    """Selection score of a kept set shared by every KV head of one (layer,
+    sequence): the fp32 sum of the H head scores, h ascending, rounded after
+    each addition (Eq. 2's sum over heads).  s_heads: (H, n).  Returns fp32 (n,)."""
+    s = np.ascontiguousarray(s_heads, dtype=np.float32)
+    H, n = s.shape
+    a = np.zeros(max(n, 1), dtype=np.float32)
+    _load().lethe_oracle_head_sum_f32(n, H, _ptr(s), _ptr(a))
+    return a[:n]
+
+
+def rasr_select_shared(s_heads, k, recent, sink):
+    """RASR keep mask shared by all KV heads of one (layer, sequence): the rule
+    of rasr_select applied to the head-summed score.  s_heads: (H, n)."""
+    return rasr_select(head_sum_f32(s_heads), k, recent, sink)
+
+
+SHRINK_NOT_TRIGGERED = -2
+SHRINK_NO_BREAKPOINT = -1
+
+
+def segmented_shrink(a, segments, tau, recent, sink, evict_threshold):
+    """Algorithm 1 (segmented token shrinking) with the size trigger on one
+    score vector a (fp32, n).  Returns (keep bool (n,), breakpoint, new
+    evict threshold); breakpoint is SHRINK_NOT_TRIGGERED when n does not
+    exceed the threshold and SHRINK_NO_BREAKPOINT when no cut qualifies."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    n = a.shape[0]
+    keep = np.zeros(max(n, 1), dtype=np.uint8)
+    lev = ctypes.c_int32(int(evict_threshold))
+    bp = _load().lethe_oracle_shrink(n, _ptr(a), int(segments), float(tau), int(recent), int(sink),
+                                     ctypes.byref(lev), _ptr(keep))
+    if bp == -3:
+        raise MemoryError("oracle shrink failed")
+    return keep[:n].astype(bool), int(bp), int(lev.value)
 
 
 def compact(rows, keep):

@@ -283,3 +283,96 @@ int lethe_oracle_select(int64_t n, const float* s, int64_t k, int32_t recent,
   free(cs);
   return 0;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Selection score of the kept set that all KV heads of one (layer, sequence)
+ * share.  Eq. 2 collapses attention over every head into one importance
+ * vector per layer, and the GQA note after it (Eq. 3) makes that vector the
+ * same for every KV head; here the per-head accumulated scores stand in for
+ * the attention and are summed over heads:
+ *   a_j = (...((s[0][j] + s[1][j]) + s[2][j]) + ...) + s[H-1][j]
+ * in fp32, h ascending, rounded after every addition.  Ranking is a decision
+ * on floats, so it is taken on exactly the fp32 values a device forms.
+ * s: [H][n] fp32 (head-major), a: [n].
+ */
+void lethe_oracle_head_sum_f32(int64_t n, int H, const float* s, float* a) {
+  for (int64_t j = 0; j < n; ++j) {
+    float acc = s[j];
+    for (int h = 1; h < H; ++h) acc = acc + s[(int64_t)h * n + j];
+    a[j] = acc;
+  }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Algorithm 1, Segmented Attention-Based Token Shrinking, for one score
+ * vector of n tokens, together with the size trigger of the System Overview
+ * (pruning starts once the cache holds more than L_evict tokens).
+ *
+ *   0. If n <= L_evict (negative L_evict counts as 0): nothing happens, every
+ *      token is kept, L_evict is unchanged; returns -2.
+ *   1. Rank all n tokens: top_values / top_indices in the order (value
+ *      descending, index ascending), +0 and -0 equal, NaN after every number.
+ *   2. Cut points c_d = floor(n * d / D) for d = 1, ..., D - 1, in that order.
+ *   3. The breakpoint is the first cut point whose head-to-cut ratio
+ *      top_values[0] / top_values[c] reaches tau.  The algorithm's test is
+ *      printed as "<= tau" but the prose asks for the point where attention
+ *      drops sharply, and with "<=" only the first cut could ever match (the
+ *      ratio never decreases along the ranking); the reading here is ">=".
+ *      The ratio is compared without rounding, as tau * v_cut <= v_head with
+ *      both sides widened to fp64 (a product of two fp32 values is exact
+ *      there).  An undefined ratio is not a breakpoint: a head that is not
+ *      positive (0, negative, NaN) or a NaN cut value.
+ *   4. Sink indices [0, sink) and recent indices [n - recent, n), clipped to
+ *      [0, n).
+ *   5. With a breakpoint c: the kept set is sink U top_indices[0 .. c) U
+ *      recent, and L_evict <- max(L_evict, c + recent).  Without one the
+ *      algorithm leaves the retained set unassigned and the prose says
+ *      pruning is delayed: every token is kept and L_evict <- 2 * L_evict.
+ *      L_evict saturates at 2^31 - 1.
+ *
+ * a: [n] fp32 scores, keep: [n] output (1 keep, 0 evict), L_evict: in/out.
+ * Returns the breakpoint (>= 0), -1 (no breakpoint), -2 (not triggered), or
+ * -3 if scratch memory could not be allocated.
+ */
+int64_t lethe_oracle_shrink(int64_t n, const float* a, int32_t D, float tau, int32_t recent,
+                            int32_t sink, int32_t* L_evict, uint8_t* keep) {
+  int64_t Lev = *L_evict > 0 ? *L_evict : 0;
+  if (n <= Lev) {
+    for (int64_t j = 0; j < n; ++j) keep[j] = 1;
+    *L_evict = (int32_t)Lev;
+    return -2;
+  }
+  cand_t* top = (cand_t*)malloc(sizeof(cand_t) * (size_t)n);
+  if (!top) return -3;
+  for (int64_t j = 0; j < n; ++j) {
+    top[j].v = a[j];
+    top[j].j = j;
+  }
+  qsort(top, (size_t)n, sizeof(cand_t), cand_cmp);
+  int64_t breakpoint = -1;
+  for (int64_t d = 1; d <= (int64_t)D - 1; ++d) {
+    int64_t c = (n * d) / D;
+    double v_head = (double)top[0].v;
+    double v_cut = (double)top[c].v;
+    int defined = v_head > 0.0 && !isnan(v_cut);
+    if (defined && (double)tau * v_cut <= v_head) {
+      breakpoint = c;
+      break;
+    }
+  }
+  int64_t r = recent < n ? recent : n;
+  int64_t sk = sink < n ? sink : n;
+  if (breakpoint >= 0) {
+    for (int64_t j = 0; j < n; ++j) keep[j] = (j < sk || j >= n - r) ? 1 : 0;
+    for (int64_t i = 0; i < breakpoint; ++i) keep[top[i].j] = 1;
+    int64_t next = breakpoint + (int64_t)recent;
+    if (next > Lev) Lev = next;
+  } else {
+    for (int64_t j = 0; j < n; ++j) keep[j] = 1;
+    Lev = 2 * Lev;
+  }
+  if (Lev > 2147483647) Lev = 2147483647;
+  *L_evict = (int32_t)Lev;
+  free(top);
+  return breakpoint;
+}
