@@ -214,6 +214,60 @@ lethe_status lethe_rasr_select(const lethe_cache* cache, const int32_t* budget, 
                                hipStream_t stream);
 
 /*
+ * RASR retention with one kept set per (layer, sequence), shared by all its KV
+ * heads: Eq. 2 collapses attention over every head into a single importance
+ * vector per layer, and the GQA note that follows it (Eq. 3) makes that
+ * vector head-invariant.  The rank key of row j is the head-summed score
+ *     a_j = (...((s_{h=0,j} + s_{1,j}) + s_{2,j}) + ...) + s_{H_KV-1,j}
+ * in fp32 (ascending heads, rounded after each addition); the keep rule is
+ * that of lethe_rasr_select applied to a with k = max(budget[b][l], 0), and
+ * the same mask is written into the keep rows of every KV head, so
+ * lethe_kv_compact then moves the same token positions in every head.
+ * Arguments, workspace and errors as lethe_rasr_select.
+ */
+lethe_status lethe_rasr_select_shared(const lethe_cache* cache, const int32_t* budget,
+                                      int32_t recent, int32_t sink, uint8_t* keep, void* ws,
+                                      size_t ws_bytes, hipStream_t stream);
+
+/* breakpoint[] values of lethe_segmented_shrink that are not cut points. */
+#define LETHE_SHRINK_NO_BREAKPOINT (-1)
+#define LETHE_SHRINK_NOT_TRIGGERED (-2)
+
+/*
+ * Algorithm 1 (Segmented Attention-Based Token Shrinking) with the size
+ * trigger of the System Overview, for every (layer l, sequence b), on the
+ * head-summed score a of lethe_rasr_select_shared (one kept set shared by the
+ * KV heads).  With n = len[l][b] and L = max(evict_threshold[l][b], 0):
+ *
+ *  0. n <= L: not triggered; every row is kept, the threshold becomes L,
+ *     breakpoint = LETHE_SHRINK_NOT_TRIGGERED.
+ *  1. Rank the n rows by (a descending, row ascending), +0 = -0, NaN last;
+ *     v[r] is the value at rank r.
+ *  2. Cut points c_d = floor(n * d / segments), d = 1 .. segments - 1.
+ *  3. The breakpoint is the first c_d whose ratio v[0] / v[c_d] reaches tau,
+ *     evaluated exactly as tau * v[c_d] <= v[0] in fp64 (the printed "<= tau"
+ *     is read as ">= tau": the prose asks for the cut where attention drops
+ *     sharply, and the ratio never falls along the ranking).  A ratio with
+ *     v[0] <= 0, v[0] NaN or v[c_d] NaN is undefined and never qualifies.
+ *  4. With a breakpoint c: keep rows [0, sink), the c best-ranked rows and
+ *     rows [n - recent, n) (windows clipped to [0, n)); the threshold becomes
+ *     max(L, c + recent).  Without one pruning is delayed: every row is kept
+ *     and the threshold becomes 2 L.  Thresholds saturate at 2^31 - 1.
+ *
+ *  segments >= 1 (1 gives no cut points); tau > 1 and finite; recent, sink >= 0.
+ *  evict_threshold int32 [num_layers][num_seqs], read and updated in place.
+ *  breakpoint int32 [num_layers][num_seqs] or NULL: the breakpoint c, or one
+ *  of the two codes above.  keep uint8 [num_layers][rows_per_layer] as for
+ *  lethe_rasr_select; lethe_kv_compact then drops the evicted rows.
+ *  ws may be NULL.  Applies a pending decode step first.  Errors:
+ *  LETHE_ERR_INVALID, LETHE_ERR_UNSUPPORTED, LETHE_ERR_HIP.
+ */
+lethe_status lethe_segmented_shrink(const lethe_cache* cache, int32_t segments, float tau,
+                                    int32_t recent, int32_t sink, int32_t* evict_threshold,
+                                    int32_t* breakpoint, uint8_t* keep, void* ws, size_t ws_bytes,
+                                    hipStream_t stream);
+
+/*
  * In-place, order-preserving compaction (pruned tokens leave the cache, as
  * the paper's System Overview and its pruning illustration describe): in
  * every segment the live rows with keep != 0 move, in order, to the front; K,

@@ -193,18 +193,10 @@ lethe_status lethe_layer_sparsity(const lethe_cache* c, const int64_t* global_bu
   return launch_sparsity(a, stream);
 }
 
-lethe_status lethe_rasr_select(const lethe_cache* c, const int32_t* budget, int32_t recent,
-                               int32_t sink, uint8_t* keep, void* ws, size_t ws_bytes,
-                               hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
-  lethe_status st = check_cache(c);
-  if (st != LETHE_OK) return st;
-  if (!budget || !keep) return LETHE_ERR_INVALID;
-  if (recent < 0 || sink < 0) return LETHE_ERR_INVALID;
-  st = flush_pending(c, stream);
-  if (st != LETHE_OK) return st;
-  SelectArgs a;
+namespace {
+
+lethe::SelectArgs select_args(const lethe_cache* c, int32_t mode, uint8_t* keep) {
+  lethe::SelectArgs a;
   a.score = c->score;
   a.len = c->len;
   a.seq_base = c->seq_base;
@@ -213,12 +205,73 @@ lethe_status lethe_rasr_select(const lethe_cache* c, const int32_t* budget, int3
   a.L = c->num_layers;
   a.B = c->num_seqs;
   a.HK = c->num_kv_heads;
+  a.mode = mode;
+  a.budget = nullptr;
+  a.recent = 0;
+  a.sink = 0;
+  a.segments = 0;
+  a.tau = 0.0f;
+  a.evict = nullptr;
+  a.breakpoint = nullptr;
+  a.keep = keep;
+  a.dev_status = c->dev_status;
+  return a;
+}
+
+lethe_status rasr_select_mode(const lethe_cache* c, const int32_t* budget, int32_t recent,
+                              int32_t sink, uint8_t* keep, int32_t mode, hipStream_t stream) {
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  if (!budget || !keep) return LETHE_ERR_INVALID;
+  if (recent < 0 || sink < 0) return LETHE_ERR_INVALID;
+  st = flush_pending(c, stream);
+  if (st != LETHE_OK) return st;
+  lethe::SelectArgs a = select_args(c, mode, keep);
   a.budget = budget;
   a.recent = recent;
   a.sink = sink;
-  a.keep = keep;
-  a.dev_status = c->dev_status;
-  return launch_select(a, stream);
+  return lethe::launch_select(a, stream);
+}
+
+}  // namespace
+
+lethe_status lethe_rasr_select(const lethe_cache* c, const int32_t* budget, int32_t recent,
+                               int32_t sink, uint8_t* keep, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  return rasr_select_mode(c, budget, recent, sink, keep, lethe::kSelectRasr, stream);
+}
+
+lethe_status lethe_rasr_select_shared(const lethe_cache* c, const int32_t* budget, int32_t recent,
+                                      int32_t sink, uint8_t* keep, void* ws, size_t ws_bytes,
+                                      hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  return rasr_select_mode(c, budget, recent, sink, keep, lethe::kSelectRasrShared, stream);
+}
+
+lethe_status lethe_segmented_shrink(const lethe_cache* c, int32_t segments, float tau,
+                                    int32_t recent, int32_t sink, int32_t* evict_threshold,
+                                    int32_t* breakpoint, uint8_t* keep, void* ws, size_t ws_bytes,
+                                    hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  if (!evict_threshold || !keep) return LETHE_ERR_INVALID;
+  if (recent < 0 || sink < 0 || segments < 1) return LETHE_ERR_INVALID;
+  if (!(tau > 1.0f) || !isfinite(tau)) return LETHE_ERR_INVALID;
+  st = flush_pending(c, stream);
+  if (st != LETHE_OK) return st;
+  lethe::SelectArgs a = select_args(c, lethe::kSelectShrink, keep);
+  a.recent = recent;
+  a.sink = sink;
+  a.segments = segments;
+  a.tau = tau;
+  a.evict = evict_threshold;
+  a.breakpoint = breakpoint;
+  return lethe::launch_select(a, stream);
 }
 
 lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* ws, size_t ws_bytes,

@@ -150,6 +150,15 @@ struct SparsityArgs {
 
 lethe_status launch_sparsity(const SparsityArgs& a, hipStream_t s);
 
+// Selection rules of launch_select.
+enum SelectMode : int32_t {
+  kSelectRasr = 0,        // RASR per (layer, sequence, KV head)
+  kSelectRasrShared = 1,  // RASR on the head-summed score, one mask per (layer, sequence)
+  kSelectShrink = 2,      // Algorithm 1 with the size trigger, head-summed score
+};
+constexpr int32_t kShrinkNoBreakpoint = -1;
+constexpr int32_t kShrinkNotTriggered = -2;
+
 struct SelectArgs {
   const float* score;
   const int32_t* len;
@@ -157,8 +166,13 @@ struct SelectArgs {
   const int32_t* cap;
   int64_t rows_per_layer;
   int32_t L, B, HK;
-  const int32_t* budget;  // [B][L]
+  int32_t mode;           // SelectMode
+  const int32_t* budget;  // [B][L], RASR modes
   int32_t recent, sink;
+  int32_t segments;       // cut points of Algorithm 1: segments - 1
+  float tau;              // Algorithm 1 ratio threshold (> 1)
+  int32_t* evict;         // [L][B] eviction thresholds, in/out (shrink)
+  int32_t* breakpoint;    // [L][B] or null (shrink)
   uint8_t* keep;
   int32_t* dev_status;
 };

@@ -1,19 +1,31 @@
-// RASR retention mask by radix selection, gfx950.
+// Retention masks by radix selection, gfx950.
 //
-// One block per (layer, sequence, KV head) segment.  The fp32 scores are mapped
-// to 32-bit keys whose unsigned order is the float order (+0 and -0 equal, NaN
-// below every number).  An MSB-first radix select with 8-bit digits and a
-// 256-bin LDS histogram finds the exact key T of the m-th best candidate and
-// how many candidates equal to T are still needed; a final ordered pass keeps
-// every candidate above T and the lowest-indexed ones equal to T.
+// Three rules share one kernel template:
+//  * RASR per segment: one block per (layer, sequence, KV head); the rank key
+//    is that head's accumulated score.
+//  * RASR shared by the heads of a layer: one block per (layer, sequence); the
+//    key is the head-summed score (Eq. 2 collapses attention over heads), the
+//    fp32 sum in ascending head order, and the mask goes to every head.
+//  * Algorithm 1 (segmented token shrinking) with the size trigger: one block
+//    per (layer, sequence) on the head-summed score.  The breakpoint needs no
+//    sort: the head-to-cut ratio test holds on a suffix of the ranking (the
+//    values never increase along it), so one max pass and one counting pass
+//    give the first rank where it holds, and the breakpoint is the first cut
+//    point at or after it.  The salient set is then the top-`breakpoint`
+//    selection below.
+//
+// Selection: fp32 keys map to 32-bit words whose unsigned order is the float
+// order (+0 and -0 equal, NaN below every number).  An MSB-first radix select
+// with 8-bit digits and a 256-bin LDS histogram finds the exact key T of the
+// m-th best candidate and how many candidates equal to T are still needed; an
+// ordered pass keeps every candidate above T and the lowest-indexed ones
+// equal to T.
 #include "device_common.h"
 #include "lethe_internal.h"
 
 namespace lethe {
 
 namespace {
-
-constexpr int kThreads = 256;
 
 __device__ inline uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f);
@@ -22,10 +34,119 @@ __device__ inline uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
-  const int h = blockIdx.x % a.HK;
-  const int b = (blockIdx.x / a.HK) % a.B;
-  const int l = blockIdx.x / (a.HK * a.B);
+// Inverse of order_key on the keys of numbers (NaN's key 0 is never inverted).
+__device__ inline float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// Rank value of row j: one head's score, or the fp32 head sum (additions in
+// ascending head order, each rounded; no multiply, so nothing contracts).
+template <bool kShared>
+struct Scores {
+  const float* s;       // head 0's segment
+  long long hstride;    // rows between the segments of consecutive heads
+  int heads;
+  __device__ inline float operator()(int j) const {
+    if constexpr (!kShared) {
+      return s[j];
+    } else {
+      float acc = s[j];
+      for (int h = 1; h < heads; ++h) acc = acc + s[h * hstride + j];
+      return acc;
+    }
+  }
+};
+
+template <int NT>
+struct SelectShared {
+  uint32_t hist[256];
+  uint32_t suffix[257];
+  uint32_t digit, need;
+  uint32_t red_u[NT / kWave];
+  uint32_t red_c[NT / kWave];
+  long long scan_tmp[NT / kWave + 1];
+  int plan[4];  // lo, hi, m, keep-all flag
+};
+
+// Key T of the m-th best key among rows [lo, hi) (m >= 1) and how many rows
+// with key T belong to the best m.  All threads get both.
+template <int NT, class KeyFn>
+__device__ void radix_select(const KeyFn& rank, int lo, int hi, uint32_t m, SelectShared<NT>& sh,
+                             uint32_t* T_out, uint32_t* need_out) {
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0, pmask = 0, need = m;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    if (tid < 256) sh.hist[tid] = 0;
+    __syncthreads();
+    for (int j = lo + tid; j < hi; j += NT) {
+      const uint32_t key = order_key(rank(j));
+      if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    // suffix[d] = matching keys whose digit is >= d: wave 0, four bins a lane.
+    if (tid < kWave) {
+      const uint32_t h0 = sh.hist[4 * tid], h1 = sh.hist[4 * tid + 1];
+      const uint32_t h2 = sh.hist[4 * tid + 2], h3 = sh.hist[4 * tid + 3];
+      const uint32_t tot = h0 + h1 + h2 + h3;
+      uint32_t incl = tot;  // sum over lanes tid .. 63
+      for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t v = __shfl_down(incl, o);
+        if (tid + o < kWave) incl += v;
+      }
+      const uint32_t above = incl - tot;
+      sh.suffix[4 * tid + 3] = above + h3;
+      sh.suffix[4 * tid + 2] = above + h3 + h2;
+      sh.suffix[4 * tid + 1] = above + h3 + h2 + h1;
+      sh.suffix[4 * tid] = incl;
+      if (tid == 0) sh.suffix[256] = 0;
+    }
+    __syncthreads();
+    if (tid < 256 && sh.suffix[tid] >= need && sh.suffix[tid + 1] < need) {
+      sh.digit = (uint32_t)tid;
+      sh.need = need - sh.suffix[tid + 1];
+    }
+    __syncthreads();
+    prefix |= sh.digit << shift;
+    pmask |= 255u << shift;
+    need = sh.need;
+    __syncthreads();
+  }
+  *T_out = prefix;
+  *need_out = need;
+}
+
+// Block-wide max of a key and sum of a count; every thread gets both.
+template <int NT>
+__device__ void block_max_count(uint32_t key, uint32_t cnt, SelectShared<NT>& sh, uint32_t* kmax,
+                                uint32_t* csum) {
+  for (int o = kWave / 2; o > 0; o >>= 1) {
+    key = max(key, (uint32_t)__shfl_xor(key, o));
+    cnt += (uint32_t)__shfl_xor(cnt, o);
+  }
+  const int w = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    sh.red_u[w] = key;
+    sh.red_c[w] = cnt;
+  }
+  __syncthreads();
+  uint32_t k = 0, c = 0;
+  for (int i = 0; i < NT / kWave; ++i) {
+    k = max(k, sh.red_u[i]);
+    c += sh.red_c[i];
+  }
+  __syncthreads();
+  *kmax = k;
+  *csum = c;
+}
+
+template <int NT, int MODE>
+__global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
+  constexpr bool kShared = MODE != kSelectRasr;
+  constexpr bool kShrink = MODE == kSelectShrink;
+  const int h = kShared ? 0 : (int)(blockIdx.x % a.HK);
+  const int lb = kShared ? (int)blockIdx.x : (int)(blockIdx.x / a.HK);
+  const int b = lb % a.B;
+  const int l = lb / a.B;
   const int tid = threadIdx.x;
   const int n = a.len[(long long)l * a.B + b];
   const int c = a.cap[b];
@@ -35,68 +156,108 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     return;
   }
   const long long row0 = (long long)l * a.rows_per_layer + base + (long long)h * c;
-  const float* s = a.score + row0;
+  const Scores<kShared> rank{a.score + row0, (long long)c, a.HK};
   uint8_t* keep = a.keep + row0;
-  int k = a.budget[(long long)b * a.L + l];
-  if (k < 0) k = 0;
-  if (k >= n) {
-    for (int j = tid; j < n; j += kThreads) keep[j] = 1;
-    return;
-  }
-  const int r = min(a.recent, k);
-  const int sk = min(a.sink, k - r);
-  const int m = k - r - sk;
-  const int lo = sk, hi = n - r;
+  const int nheads = kShared ? a.HK : 1;
+  __shared__ SelectShared<NT> sh;
 
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t suffix[257];
-  __shared__ uint32_t s_digit, s_need;
-  __shared__ long long scan_tmp[kThreads / kWave + 1];
-
-  uint32_t prefix = 0, pmask = 0, need = (uint32_t)m;
-  if (m > 0) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      hist[tid] = 0;
-      __syncthreads();
-      for (int j = lo + tid; j < hi; j += kThreads) {
-        uint32_t key = order_key(s[j]);
-        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+  // Plan: candidate rows [lo, hi), how many of them to keep (m), and the
+  // forced rows, which are [0, fs) and [fr, n).
+  int lo = 0, hi = 0, m = 0, fs = 0, fr = n;
+  bool all = false;
+  if constexpr (!kShrink) {
+    int k = a.budget[(long long)b * a.L + l];
+    if (k < 0) k = 0;
+    if (k >= n) {
+      all = true;
+    } else {
+      const int r = min(a.recent, k);
+      const int sk = min(a.sink, k - r);
+      m = k - r - sk;
+      lo = sk;
+      hi = n - r;
+      fs = sk;
+      fr = n - r;
+    }
+  } else {
+    const long long lev0 = max(a.evict[(long long)l * a.B + b], 0);
+    long long lev = lev0;
+    long long bp = kShrinkNotTriggered;
+    if (n <= lev0) {
+      all = true;
+    } else {
+      // Head of the ranking and the NaN count.
+      uint32_t kmax = 0, nnan = 0;
+      {
+        uint32_t km = 0, cn = 0;
+        for (int j = tid; j < n; j += NT) {
+          const float v = rank(j);
+          km = max(km, order_key(v));
+          cn += (v != v) ? 1u : 0u;
+        }
+        block_max_count<NT>(km, cn, sh, &kmax, &nnan);
       }
-      __syncthreads();
-      // suffix[d] = number of matching candidates whose digit is >= d.
-      if (tid == 0) {
-        uint32_t acc = 0;
-        suffix[256] = 0;
-        for (int d = 255; d >= 0; --d) {
-          acc += hist[d];
-          suffix[d] = acc;
+      bp = kShrinkNoBreakpoint;
+      const float head = key_value(kmax);
+      if (kmax != 0u && head > 0.0f && a.segments > 1) {
+        // cnt = rows whose ratio head / value stays below tau (tau * value >
+        // head, exact in fp64): ranks [cnt, n - nnan) pass the test.
+        const double dh = (double)head, dt = (double)a.tau;
+        uint32_t cn = 0, unused = 0;
+        for (int j = tid; j < n; j += NT) {
+          const float v = rank(j);
+          cn += (v == v && dt * (double)v > dh) ? 1u : 0u;
+        }
+        uint32_t cnt = 0;
+        block_max_count<NT>(0u, cn, sh, &unused, &cnt);
+        const long long D = a.segments;
+        long long d = ((long long)cnt * D + n - 1) / n;  // first d with n*d >= cnt*D
+        if (d < 1) d = 1;
+        if (d <= D - 1) {
+          const long long cut = ((long long)n * d) / D;
+          if (cut < (long long)n - (long long)nnan) bp = cut;
         }
       }
-      __syncthreads();
-      if (suffix[tid] >= need && suffix[tid + 1] < need) {
-        s_digit = (uint32_t)tid;
-        s_need = need - suffix[tid + 1];
+      if (bp >= 0) {
+        m = (int)bp;
+        lo = 0;
+        hi = n;
+        fs = min(a.sink, n);
+        fr = n - min(a.recent, n);
+        lev = max(lev0, bp + (long long)a.recent);
+      } else {
+        all = true;
+        lev = 2 * lev0;
       }
-      __syncthreads();
-      prefix |= s_digit << shift;
-      pmask |= 255u << shift;
-      need = s_need;
-      __syncthreads();
+      if (lev > 0x7fffffffLL) lev = 0x7fffffffLL;
+    }
+    if (tid == 0) {
+      a.evict[(long long)l * a.B + b] = (int32_t)lev;
+      if (a.breakpoint) a.breakpoint[(long long)l * a.B + b] = (int32_t)bp;
     }
   }
-  const uint32_t T = prefix;
+
+  if (all) {
+    for (int hh = 0; hh < nheads; ++hh)
+      for (int j = tid; j < n; j += NT) keep[(long long)hh * c + j] = 1;
+    return;
+  }
+  uint32_t T = 0, need = 0;
+  if (m > 0) radix_select<NT>(rank, lo, hi, (uint32_t)m, sh, &T, &need);
   // Ordered pass: ties with key T are taken by increasing row index.
   long long carry = 0;
-  for (int j0 = 0; j0 < n; j0 += kThreads) {
+  for (int j0 = 0; j0 < n; j0 += NT) {
     const int j = j0 + tid;
-    bool cand = j >= lo && j < hi && j < n;
-    uint32_t key = cand ? order_key(s[j]) : 0u;
-    bool eq = cand && m > 0 && key == T;
+    const bool cand = j >= lo && j < hi && j < n;
+    const uint32_t key = (cand && m > 0) ? order_key(rank(j)) : 0u;
+    const bool eq = cand && m > 0 && key == T;
     long long total;
-    long long rank = block_excl_scan<kThreads>(eq ? 1 : 0, scan_tmp, &total);
+    const long long pos = block_excl_scan<NT>(eq ? 1 : 0, sh.scan_tmp, &total);
     if (j < n) {
-      bool kp = !cand || (m > 0 && (key > T || (eq && carry + rank < (long long)need)));
-      keep[j] = kp ? 1 : 0;
+      const bool forced = j < fs || j >= fr;
+      const bool chosen = cand && m > 0 && (key > T || (eq && carry + pos < (long long)need));
+      const uint8_t kp = (forced || chosen) ? 1 : 0;
+      for (int hh = 0; hh < nheads; ++hh) keep[(long long)hh * c + j] = kp;
     }
     carry += total;
   }
@@ -105,9 +266,22 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
 }  // namespace
 
 lethe_status launch_select(const SelectArgs& a, hipStream_t s) {
-  long long nb = (long long)a.L * a.B * a.HK;
+  const long long nb = (long long)a.L * a.B * (a.mode == kSelectRasr ? a.HK : 1);
   if (nb > 0x7fffffffLL) return LETHE_ERR_UNSUPPORTED;
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)nb), dim3(kThreads), 0, s, a);
+  if (nb == 0) return LETHE_OK;
+  switch (a.mode) {
+    case kSelectRasr:
+      hipLaunchKernelGGL((select_kernel<256, kSelectRasr>), dim3((unsigned)nb), dim3(256), 0, s, a);
+      break;
+    case kSelectRasrShared:
+      hipLaunchKernelGGL((select_kernel<1024, kSelectRasrShared>), dim3((unsigned)nb), dim3(1024), 0, s, a);
+      break;
+    case kSelectShrink:
+      hipLaunchKernelGGL((select_kernel<1024, kSelectShrink>), dim3((unsigned)nb), dim3(1024), 0, s, a);
+      break;
+    default:
+      return LETHE_ERR_INVALID;
+  }
   if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
   return LETHE_OK;
 }

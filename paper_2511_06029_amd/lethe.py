@@ -16,8 +16,11 @@ BF16, F32 = 0, 1
 DEV_APPEND_OVERFLOW, DEV_INFEASIBLE, DEV_BAD_LAYOUT, DEV_HEAD_MISMATCH = 1, 2, 4, 8
 OP_DECODE, OP_SPARSITY, OP_SELECT, OP_COMPACT = 0, 1, 2, 3
 
+SHRINK_NO_BREAKPOINT, SHRINK_NOT_TRIGGERED = -1, -2
+
 EXPORTED = ("lethe_workspace_bytes", "lethe_state_bytes", "lethe_decode_attn_score",
-            "lethe_layer_sparsity", "lethe_rasr_select", "lethe_kv_compact", "lethe_score_flush",
+            "lethe_layer_sparsity", "lethe_rasr_select", "lethe_rasr_select_shared",
+            "lethe_segmented_shrink", "lethe_kv_compact", "lethe_score_flush",
             "lethe_status_string")
 
 
@@ -64,6 +67,10 @@ def load():
         lib.lethe_layer_sparsity.restype = ctypes.c_int
         lib.lethe_rasr_select.argtypes = [pc, vp, i32, i32, vp, vp, sz, vp]
         lib.lethe_rasr_select.restype = ctypes.c_int
+        lib.lethe_rasr_select_shared.argtypes = [pc, vp, i32, i32, vp, vp, sz, vp]
+        lib.lethe_rasr_select_shared.restype = ctypes.c_int
+        lib.lethe_segmented_shrink.argtypes = [pc, i32, ctypes.c_float, i32, i32, vp, vp, vp, vp, sz, vp]
+        lib.lethe_segmented_shrink.restype = ctypes.c_int
         lib.lethe_kv_compact.argtypes = [pc, vp, vp, sz, vp]
         lib.lethe_kv_compact.restype = ctypes.c_int
         lib.lethe_status_string.argtypes = [ctypes.c_int]
@@ -133,6 +140,26 @@ def rasr_select(cache, budget, recent, sink, keep, ws=None, stream=None):
     st = load().lethe_rasr_select(ctypes.byref(cache.c_struct()), _p(budget), int(recent), int(sink), _p(keep),
                                   _p(ws), nbytes, _stream(stream))
     _check("lethe_rasr_select", st)
+
+
+def rasr_select_shared(cache, budget, recent, sink, keep, ws=None, stream=None):
+    """lethe_rasr_select_shared: one keep mask per (layer, sequence) from the
+    head-summed score, written for every KV head."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    st = load().lethe_rasr_select_shared(ctypes.byref(cache.c_struct()), _p(budget), int(recent), int(sink),
+                                         _p(keep), _p(ws), nbytes, _stream(stream))
+    _check("lethe_rasr_select_shared", st)
+
+
+def segmented_shrink(cache, segments, tau, recent, sink, evict_threshold, breakpoint, keep, ws=None,
+                     stream=None):
+    """lethe_segmented_shrink: Algorithm 1 with the size trigger; updates
+    evict_threshold (int32 [L][B]) in place, fills breakpoint (or None)."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    st = load().lethe_segmented_shrink(ctypes.byref(cache.c_struct()), int(segments), float(tau), int(recent),
+                                       int(sink), _p(evict_threshold), _p(breakpoint), _p(keep), _p(ws), nbytes,
+                                       _stream(stream))
+    _check("lethe_segmented_shrink", st)
 
 
 def kv_compact(cache, keep, ws, stream=None):

@@ -81,6 +81,8 @@ def test_cache_validation(field, value, want):
     assert decode(c, wsb=1 << 40) == want
     lib = L.load()
     assert lib.lethe_rasr_select(ctypes.byref(c), FAKE, 8, 0, FAKE, None, 0, None) == want
+    assert lib.lethe_rasr_select_shared(ctypes.byref(c), FAKE, 8, 0, FAKE, None, 0, None) == want
+    assert lib.lethe_segmented_shrink(ctypes.byref(c), 10, 400.0, 8, 0, FAKE, None, FAKE, None, 0, None) == want
     assert lib.lethe_kv_compact(ctypes.byref(c), FAKE, FAKE, 1 << 40, None) == want
     assert lib.lethe_layer_sparsity(ctypes.byref(c), FAKE, 8, 0, None, FAKE, FAKE, None, 0, None) == want
 
@@ -117,6 +119,19 @@ def test_prune_argument_validation():
     assert lib.lethe_rasr_select(cc, FAKE, 8, 0, None, None, 0, None) == L.ERR_INVALID
     assert lib.lethe_rasr_select(cc, FAKE, -8, 0, FAKE, None, 0, None) == L.ERR_INVALID
     assert lib.lethe_rasr_select(cc, FAKE, 8, -1, FAKE, None, 0, None) == L.ERR_INVALID
+    assert lib.lethe_rasr_select_shared(cc, None, 8, 0, FAKE, None, 0, None) == L.ERR_INVALID
+    assert lib.lethe_rasr_select_shared(cc, FAKE, 8, 0, None, None, 0, None) == L.ERR_INVALID
+    assert lib.lethe_rasr_select_shared(cc, FAKE, -1, 0, FAKE, None, 0, None) == L.ERR_INVALID
+    assert lib.lethe_rasr_select_shared(cc, FAKE, 8, -1, FAKE, None, 0, None) == L.ERR_INVALID
+    shrink = lib.lethe_segmented_shrink
+    assert shrink(cc, 10, 400.0, 8, 0, None, None, FAKE, None, 0, None) == L.ERR_INVALID   # thresholds
+    assert shrink(cc, 10, 400.0, 8, 0, FAKE, None, None, None, 0, None) == L.ERR_INVALID   # keep
+    for seg in (0, -3):
+        assert shrink(cc, seg, 400.0, 8, 0, FAKE, None, FAKE, None, 0, None) == L.ERR_INVALID
+    for tau in (1.0, 0.5, -2.0, math.nan, math.inf):
+        assert shrink(cc, 10, tau, 8, 0, FAKE, None, FAKE, None, 0, None) == L.ERR_INVALID
+    assert shrink(cc, 10, 400.0, -1, 0, FAKE, None, FAKE, None, 0, None) == L.ERR_INVALID
+    assert shrink(cc, 10, 400.0, 8, -1, FAKE, None, FAKE, None, 0, None) == L.ERR_INVALID
     assert lib.lethe_kv_compact(cc, None, FAKE, 1 << 20, None) == L.ERR_INVALID
     assert lib.lethe_kv_compact(cc, FAKE, None, 1 << 20, None) == L.ERR_INVALID
     need = lib.lethe_workspace_bytes(cc, L.OP_COMPACT)
