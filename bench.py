@@ -9,10 +9,18 @@ a prune round every 512 decode steps with a recent window of 128.
 
 One benchmark step is one prune interval: 512 decode steps over all 32 layers
 (append + fused attention and Eq. 5 score update: lethe_decode_attn_score),
-then one prune round over all layers (lethe_layer_sparsity, lethe_rasr_select,
-lethe_kv_compact).  The default run (1 warm-up step + 15 timed steps) covers
-the 8192 generated tokens of the workload; inputs are resident in HBM before
-the timed region starts.
+then one prune round over all layers.  The default run (1 warm-up step + 15
+timed steps) covers the 8192 generated tokens of the workload; inputs are
+resident in HBM before the timed region starts.
+
+Prune rounds (--policy):
+  lethe         lethe_layer_sparsity, lethe_rasr_select (a kept set per KV
+                head), lethe_kv_compact -- the default, the headline line;
+  lethe-shared  the same with lethe_rasr_select_shared (one kept set per
+                layer and sequence, ranked by the head-summed score);
+  shrink        lethe_segmented_shrink (Algorithm 1 with the size trigger:
+                --segments cut points, ratio --tau, first threshold the
+                prompt length) and lethe_kv_compact.
 
 The JSON line reports KV tokens scanned per second (one token = one cached
 (layer, sequence, position) row, all KV heads) over the whole timed run, the
@@ -48,6 +56,9 @@ def parse():
     ap.add_argument("--interval", type=int, default=None, help="decode steps per prune interval (512)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--policy", choices=("lethe", "lethe-shared", "shrink"), default="lethe")
+    ap.add_argument("--segments", type=int, default=10, help="Algorithm 1 segments D (shrink)")
+    ap.add_argument("--tau", type=float, default=400.0, help="Algorithm 1 ratio threshold (shrink)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="first copy MIB MiB device-to-device 3 times (counter calibration runs)")
     return ap.parse_args()
@@ -107,6 +118,7 @@ def main():
     bud = torch.empty((B, Lyr), dtype=torch.int32, device=dev)
     keep = torch.empty((Lyr, cache.rows_per_layer), dtype=torch.uint8, device=dev)
     gbud = torch.empty(B, dtype=torch.int64, device=dev)
+    evict = torch.full((Lyr, B), T0, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
     if args.copy_probe > 0:
         # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings
@@ -131,7 +143,7 @@ def main():
     v_ptr = [[ctypes.c_void_p(vp[t, l].data_ptr()) for l in range(Lyr)] for t in range(P)]
 
     len_snap = [torch.empty((Lyr, B), dtype=torch.int32, pin_memory=True) for _ in range(windows + 1)]
-    win_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(windows)]
+    win_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(windows)]
 
     def run_window(w, timed):
         T_start = T0 + w * interval
@@ -145,11 +157,21 @@ def main():
                     raise RuntimeError("lethe_decode_attn_score: %s" % L.status_string(rc))
         win_ev[w][1].record(stream)
         T_end = T_start + interval
-        gbud.fill_(int(math.floor(cfg.budget_frac * T_end)) * Lyr)
-        L.layer_sparsity(cache, gbud, recent, sink, None, S, bud)
-        L.rasr_select(cache, bud, recent, sink, keep)
+        if args.policy == "shrink":
+            L.score_flush(cache)
+            win_ev[w][2].record(stream)
+            L.segmented_shrink(cache, args.segments, args.tau, recent, sink, evict, None, keep)
+        else:
+            gbud.fill_(int(math.floor(cfg.budget_frac * T_end)) * Lyr)
+            L.layer_sparsity(cache, gbud, recent, sink, None, S, bud)
+            win_ev[w][2].record(stream)
+            if args.policy == "lethe":
+                L.rasr_select(cache, bud, recent, sink, keep)
+            else:
+                L.rasr_select_shared(cache, bud, recent, sink, keep)
+        win_ev[w][3].record(stream)
         L.kv_compact(cache, keep, ws_c)
-        win_ev[w][2].record(stream)
+        win_ev[w][4].record(stream)
 
     log("warm-up: %d interval(s) of %d decode steps" % (args.warmup, interval))
     for w in range(args.warmup):
@@ -178,7 +200,8 @@ def main():
         tokens += interval * int(n0.sum()) + Lyr * B * interval * (interval + 1) // 2
     elapsed = t1 - t0
     decode_ms = [win_ev[w][0].elapsed_time(win_ev[w][1]) for w in range(args.warmup, windows)]
-    prune_ms = [win_ev[w][1].elapsed_time(win_ev[w][2]) for w in range(args.warmup, windows)]
+    prune_ms = [win_ev[w][1].elapsed_time(win_ev[w][4]) for w in range(args.warmup, windows)]
+    select_ms = [win_ev[w][2].elapsed_time(win_ev[w][3]) for w in range(args.warmup, windows)]
     # Roofline of lethe_decode_attn_score: one kernel launch per call, back to
     # back on the launch stream; the events bracket every decode call of the
     # timed intervals, so their span / calls is the average launch duration.
@@ -188,7 +211,21 @@ def main():
     achieved = avg_call_bytes / avg_call_s / 1e9
     traffic = load_traffic(avg_call_bytes)
 
+    # Selection reads every live score once per KV head and writes a mask
+    # byte per row and head (lengths at the end of each interval, before
+    # compaction).
+    sel_rows = 0
+    for w in range(args.warmup, windows):
+        sel_rows += int(len_snap[w].numpy().astype(np.int64).sum()) + Lyr * B * interval
+    select_gbs = sel_rows * HK * 5 / (float(np.sum(select_ms)) / 1e3) / 1e9
+
     value = tokens / elapsed
+    workload = "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128"
+    if args.policy == "lethe-shared":
+        workload += ", one kept set per layer and sequence"
+    elif args.policy == "shrink":
+        workload = ("llama3-8b-shapes batch 8, 2k prompt + generated tokens, Algorithm 1 shrinking every 512 "
+                    "(D=%d, tau=%g, recent 128, first threshold 2048)" % (args.segments, args.tau))
     result = {
         "metric": "KV tokens scanned/s (fused decode-attn+score, prune rounds included)",
         "value": value,
@@ -203,12 +240,15 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded Zipf key-bias caches, random queries)",
         "config": {
-            "workload": "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128",
+            "workload": workload,
             "layers": Lyr, "q_heads": HQ, "kv_heads": HK, "head_dim": D, "batch": B, "storage": "bf16",
             "prompt": T0, "generated": interval * windows, "interval": interval, "gamma": gamma,
         },
         "decode_step_ms": float(np.mean(decode_ms)) / interval,
         "prune_round_us": float(np.mean(prune_ms)) * 1e3,
+        "policy": args.policy,
+        "select_us": float(np.mean(select_ms)) * 1e3,
+        "select_hbm_gbs": select_gbs,
         "decode_call_us": avg_call_s * 1e6,
         "decode_hbm_gbs": achieved,
         "roofline": {
