@@ -20,7 +20,12 @@ Prune rounds (--policy):
                 layer and sequence, ranked by the head-summed score);
   shrink        lethe_segmented_shrink (Algorithm 1 with the size trigger:
                 --segments cut points, ratio --tau, first threshold the
-                prompt length) and lethe_kv_compact.
+                prompt length) and lethe_kv_compact;
+  h2o, streaming, pyramid
+                the baselines as parameterisations of the same calls
+                (paper_2511_06029_amd/policies.py): cumulative scores and
+                uniform layer budgets; sinks plus a window filling the
+                budget; PyramidKV's static layer budgets.  Same 40% budget.
 
 The JSON line reports KV tokens scanned per second (one token = one cached
 (layer, sequence, position) row, all KV heads) over the whole timed run, the
@@ -56,7 +61,8 @@ def parse():
     ap.add_argument("--interval", type=int, default=None, help="decode steps per prune interval (512)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--policy", choices=("lethe", "lethe-shared", "shrink"), default="lethe")
+    ap.add_argument("--policy", choices=("lethe", "lethe-shared", "shrink", "h2o", "streaming", "pyramid"),
+                    default="lethe")
     ap.add_argument("--segments", type=int, default=10, help="Algorithm 1 segments D (shrink)")
     ap.add_argument("--tau", type=float, default=400.0, help="Algorithm 1 ratio threshold (shrink)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -74,6 +80,7 @@ def main():
     import torch
 
     from paper_2511_06029_amd import lethe as L
+    from paper_2511_06029_amd import policies
     from workloads import CONFIGS
     from workloads.synth import ZipfCache
 
@@ -85,8 +92,9 @@ def main():
     windows = args.warmup + args.steps
     T0 = cfg.prompt
     cap = T0 + interval * windows
-    gamma = cfg.gamma
     recent, sink = cfg.recent, cfg.sink
+    policy = None if args.policy == "shrink" else policies.get(args.policy, gamma=cfg.gamma, sink=sink)
+    gamma = policy.gamma if policy else cfg.gamma
 
     def log(msg):
         print("[bench] " + msg, file=sys.stderr, flush=True)
@@ -114,10 +122,8 @@ def main():
     out = torch.empty((B, HQ, D), dtype=torch.float32, device=dev)
     ws = cache.workspace(L.OP_DECODE)
     ws_c = cache.workspace(L.OP_COMPACT)
-    S = torch.empty((B, Lyr), dtype=torch.float32, device=dev)
-    bud = torch.empty((B, Lyr), dtype=torch.int32, device=dev)
     keep = torch.empty((Lyr, cache.rows_per_layer), dtype=torch.uint8, device=dev)
-    gbud = torch.empty(B, dtype=torch.int64, device=dev)
+    prune = policies.PruneRound(cache, policy) if policy else None
     evict = torch.full((Lyr, B), T0, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
     if args.copy_probe > 0:
@@ -161,16 +167,14 @@ def main():
             L.score_flush(cache)
             win_ev[w][2].record(stream)
             L.segmented_shrink(cache, args.segments, args.tau, recent, sink, evict, None, keep)
+            win_ev[w][3].record(stream)
+            L.kv_compact(cache, keep, ws_c)
         else:
-            gbud.fill_(int(math.floor(cfg.budget_frac * T_end)) * Lyr)
-            L.layer_sparsity(cache, gbud, recent, sink, None, S, bud)
+            r, sk = prune.budgets(policies.per_layer_budget(cfg.budget_frac, T_end), recent)
             win_ev[w][2].record(stream)
-            if args.policy == "lethe":
-                L.rasr_select(cache, bud, recent, sink, keep)
-            else:
-                L.rasr_select_shared(cache, bud, recent, sink, keep)
-        win_ev[w][3].record(stream)
-        L.kv_compact(cache, keep, ws_c)
+            prune.select(r, sk)
+            win_ev[w][3].record(stream)
+            prune.compact()
         win_ev[w][4].record(stream)
 
     log("warm-up: %d interval(s) of %d decode steps" % (args.warmup, interval))
@@ -223,6 +227,8 @@ def main():
     workload = "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128"
     if args.policy == "lethe-shared":
         workload += ", one kept set per layer and sequence"
+    elif args.policy in ("h2o", "streaming", "pyramid"):
+        workload = workload.replace("40% budget", "40%% budget, %s rule" % args.policy)
     elif args.policy == "shrink":
         workload = ("llama3-8b-shapes batch 8, 2k prompt + generated tokens, Algorithm 1 shrinking every 512 "
                     "(D=%d, tau=%g, recent 128, first threshold 2048)" % (args.segments, args.tau))

@@ -154,6 +154,18 @@ def segmented_shrink(a, segments, tau, recent, sink, evict_threshold):
     return keep[:n].astype(bool), int(bp), int(lev.value)
 
 
+def pyramid_budgets(L, total, beta):
+    """PyramidKV's per-layer budgets (a baseline the paper compares against):
+    an arithmetic progression falling with depth, whose last layer holds
+    total / (beta * L) and whose first holds 2 total / L minus that, so the L
+    budgets sum to total.  Real-valued (fp64), one per layer."""
+    last = total / (beta * L)
+    first = 2.0 * total / L - last
+    if L == 1:
+        return [float(total)]
+    return [first - l * (first - last) / (L - 1) for l in range(L)]
+
+
 def compact(rows, keep):
     """Order-preserving compaction: the kept rows, in their original order."""
     keep = np.asarray(keep, dtype=bool)

@@ -247,3 +247,19 @@ def test_shrink_scale_invariant_by_powers_of_two():
         got = oracle.segmented_shrink(a * np.float32(2.0 ** e), 10, 30.0, 16, 4, 0)
         np.testing.assert_array_equal(got[0], base[0])
         assert got[1:] == base[1:]
+
+
+# --------------------------------------------------------------------------
+# Baseline policies: PyramidKV's layer budgets
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("L,total,beta", [(32, 32 * 1000, 20.0), (28, 5000, 10.0), (2, 100, 4.0), (1, 77, 20.0)])
+def test_pyramid_budgets_progression(L, total, beta):
+    k = oracle.pyramid_budgets(L, total, beta)
+    assert len(k) == L
+    assert abs(sum(k) - total) <= 1e-9 * total          # the budgets add up to the total
+    if L > 1:
+        assert abs(k[-1] - total / (beta * L)) <= 1e-9 * total
+        steps = np.diff(k)
+        assert np.all(steps < 0) and np.allclose(steps, steps[0])   # linear, falling with depth
+        assert abs(k[0] / k[-1] - (2 * beta - 1)) <= 1e-9 * beta    # first : last = 2 beta - 1
