@@ -1,7 +1,8 @@
 """oracle -- TEST INFRASTRUCTURE ONLY.
 
 Plain, slow CPU reference for the Lethe hot path (arXiv 2511.06029): decode
-attention with importance accumulation (Eq. 5), per-layer Hoyer sparsity
+attention with importance accumulation (Eq. 5), causal prefill attention that
+seeds the importance (Eq. 2 over the prompt's queries), per-layer Hoyer sparsity
 (Eq. 1 on the head-summed score of Eq. 2), the layer budget split, RASR
 retention (per KV head, or shared by the heads of a layer), Algorithm 1's
 segmented shrinking with its size trigger, and order-preserving compaction.
@@ -44,6 +45,8 @@ def _load():
         lib.lethe_oracle_head_sum_f32.restype = None
         lib.lethe_oracle_shrink.argtypes = [i64, vp, i32, ctypes.c_float, i32, i32, vp, vp]
         lib.lethe_oracle_shrink.restype = i64
+        lib.lethe_oracle_prefill.argtypes = [i64, i64, ctypes.c_int, ctypes.c_int, vp, vp, vp, dbl, vp, vp, vp]
+        lib.lethe_oracle_prefill.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -76,6 +79,33 @@ def attend(q, K, V, s_in, gamma, scale):
     if rc != 0:
         raise MemoryError("oracle attend failed")
     return out, s_out
+
+
+def prefill(q, K, V, s_in, scale):
+    """Causal prefill attention of the qlen newest rows of one KV segment for
+    the G query heads of its group, plus Eq. 2's importance (attention summed
+    over the heads and the queries) added to s_in.
+
+    q: (qlen, G, D); K, V: (n, D); s_in: (n,) or None.  Returns (out (qlen, G,
+    D) float64, s_out (n,) float64)."""
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    K = np.ascontiguousarray(K, dtype=np.float32)
+    V = np.ascontiguousarray(V, dtype=np.float32)
+    qlen, G, D = q.shape
+    n = K.shape[0]
+    assert K.shape == (n, D) and V.shape == (n, D)
+    out = np.zeros((max(qlen, 1), G, D), dtype=np.float64)
+    s_out = np.zeros(max(n, 1), dtype=np.float64)
+    sp = None
+    if s_in is not None:
+        s_in = np.ascontiguousarray(s_in, dtype=np.float64)
+        assert s_in.shape == (n,)
+        sp = _ptr(s_in)
+    rc = _load().lethe_oracle_prefill(n, qlen, D, G, _ptr(q), _ptr(K), _ptr(V), float(scale), sp,
+                                      _ptr(s_out), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle prefill failed (%d)" % rc)
+    return out[:qlen], s_out[:n]
 
 
 def hoyer(a):

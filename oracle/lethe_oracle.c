@@ -376,3 +376,56 @@ int64_t lethe_oracle_shrink(int64_t n, const float* a, int32_t D, float tau, int
   free(top);
   return breakpoint;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Prefill attention with score seeding for one segment: the qlen newest of
+ * the segment's n cached rows come with queries (a prompt, or one chunk of
+ * it).  Query i sits at position p = n - qlen + i and attends, causally, to
+ * rows 0 .. p.  For each query head g of the KV group (ascending) and each
+ * query i (ascending), as plain softmax attention:
+ *   x_j  = scale * sum_d q[i][g][d] * K[j][d]          (d ascending), j <= p
+ *   m    = max_j x_j,  l = sum_j exp(x_j - m),  p_j = exp(x_j - m) / l
+ *   out[i][g][d] = sum_j p_j * V[j][d]                  (j ascending)
+ * and the importance of Eq. 2 (attention summed over query heads and query
+ * positions, here over the G heads of the group and the qlen queries):
+ *   s_out[j] = s_in[j] + sum_g sum_i p_{g,i,j}          (g, then i ascending)
+ * No decay between the queries of one call: they are one observation.
+ *
+ * q: [qlen][G][D], K and V: [n][D], s_in: [n] or NULL (zero), s_out: [n],
+ * out: [qlen][G][D].  Requires 0 <= qlen <= n.  Returns 0, -1 on bad sizes,
+ * -2 if scratch memory could not be allocated.
+ */
+int lethe_oracle_prefill(int64_t n, int64_t qlen, int D, int G, const float* q, const float* K,
+                         const float* V, double scale, const double* s_in, double* s_out,
+                         double* out) {
+  if (qlen < 0 || qlen > n) return -1;
+  for (int64_t j = 0; j < n; ++j) s_out[j] = s_in ? s_in[j] : 0.0;
+  for (int64_t e = 0; e < qlen * G * D; ++e) out[e] = 0.0;
+  if (qlen == 0) return 0;
+  double* x = (double*)malloc(sizeof(double) * (size_t)n);
+  if (!x) return -2;
+  for (int g = 0; g < G; ++g) {
+    for (int64_t i = 0; i < qlen; ++i) {
+      const int64_t p = n - qlen + i;
+      const float* qi = q + (i * G + g) * D;
+      for (int64_t j = 0; j <= p; ++j) {
+        double acc = 0.0;
+        for (int d = 0; d < D; ++d) acc += (double)qi[d] * (double)K[j * D + d];
+        x[j] = scale * acc;
+      }
+      double m = x[0];
+      for (int64_t j = 1; j <= p; ++j)
+        if (x[j] > m || isnan(x[j])) m = x[j];
+      double l = 0.0;
+      for (int64_t j = 0; j <= p; ++j) l += exp(x[j] - m);
+      double* oi = out + (i * G + g) * D;
+      for (int64_t j = 0; j <= p; ++j) {
+        double pj = exp(x[j] - m) / l;
+        for (int d = 0; d < D; ++d) oi[d] += pj * (double)V[j * D + d];
+        s_out[j] += pj;
+      }
+    }
+  }
+  free(x);
+  return 0;
+}
