@@ -165,6 +165,46 @@ lethe_status lethe_decode_attn_score(const lethe_cache* cache, int32_t layer, co
                                      hipStream_t stream);
 
 /*
+ * Causal prefill attention that seeds the importance scores, for one layer.
+ * Eq. 2 collapses attention over heads and query positions into one
+ * importance vector; here the sum runs over the query heads of each KV group
+ * (as in lethe_decode_attn_score) and over the call's queries.
+ *
+ * Sequence b comes with q_len[b] queries, for the q_len[b] newest of its
+ * n = len[layer][b] cached rows (the prompt, or one chunk of it, whose K and
+ * V the caller has already written into the cache).  Query i sits at position
+ * p = n - q_len[b] + i and attends rows 0 .. p.  For query head j = h G + g:
+ *     x = softmax_scale * q[row][j][:] . K[0..p][:],  P = softmax(x),
+ *     out[row][j][:] = sum_r P_r V[r][:]           (row = q_start[b] + i)
+ * and for every row r < n of every KV head h:
+ *     s_r <- s_r + sum_{g < G} sum_i P_{hG+g, i, r}
+ * No decay between the queries of one call; later decode steps decay the
+ * seeded scores as Eq. 5 says.  Chunked prefill (several calls covering
+ * consecutive chunks) gives the same outputs and scores as one call.
+ *
+ *  q        bf16 [q_rows][num_q_heads][head_dim]; out fp32, same layout.
+ *  q_start  int64 [num_seqs], q_len int32 [num_seqs] (device): the rows of
+ *           sequence b are q_start[b] .. q_start[b] + q_len[b] - 1.
+ *  max_q_len, max_kv_len  host upper bounds of q_len[b] and len[layer][b]
+ *           (they size the grid).
+ *  ws       lethe_prefill_workspace_bytes(cache, q_rows) bytes (per query
+ *           row and head: the softmax max and 1 / sum between the passes).
+ * A sequence whose sizes do not fit (q_len > len, a bound exceeded, rows
+ * outside [0, q_rows), a bad layout) sets LETHE_DEV_BAD_LAYOUT and is left
+ * untouched.  Applies a pending decode step first.  bf16 caches only
+ * (LETHE_ERR_UNSUPPORTED otherwise).  Accumulation fp32, P kept to fp32
+ * accuracy in the P V product.  Errors: LETHE_ERR_INVALID, LETHE_ERR_UNSUPPORTED,
+ * LETHE_ERR_WORKSPACE, LETHE_ERR_HIP.
+ */
+lethe_status lethe_prefill_attn_score(const lethe_cache* cache, int32_t layer, const void* q,
+                                      const int64_t* q_start, const int32_t* q_len, int64_t q_rows,
+                                      int32_t max_q_len, int32_t max_kv_len, float softmax_scale,
+                                      float* out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes lethe_prefill_attn_score needs for q_rows query rows. */
+size_t lethe_prefill_workspace_bytes(const lethe_cache* cache, int64_t q_rows);
+
+/*
  * Layer sparsity and budgets for every sequence (start of a prune round).
  *
  *  Applies a pending decode step first (as lethe_score_flush).

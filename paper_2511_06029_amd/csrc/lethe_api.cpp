@@ -274,6 +274,56 @@ lethe_status lethe_segmented_shrink(const lethe_cache* c, int32_t segments, floa
   return lethe::launch_select(a, stream);
 }
 
+size_t lethe_prefill_workspace_bytes(const lethe_cache* c, int64_t q_rows) {
+  if (!c || q_rows < 0 || c->num_q_heads <= 0) return 0;
+  return align_up((size_t)q_rows * (size_t)c->num_q_heads * 2 * sizeof(float), 256);
+}
+
+lethe_status lethe_prefill_attn_score(const lethe_cache* c, int32_t layer, const void* q,
+                                      const int64_t* q_start, const int32_t* q_len, int64_t q_rows,
+                                      int32_t max_q_len, int32_t max_kv_len, float softmax_scale,
+                                      float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  if (c->dtype != LETHE_BF16) return LETHE_ERR_UNSUPPORTED;
+  if (layer < 0 || layer >= c->num_layers) return LETHE_ERR_INVALID;
+  if (!q_start || !q_len || q_rows < 0 || max_q_len < 0 || max_kv_len < 0) return LETHE_ERR_INVALID;
+  if (q_rows > 0 && (!q || !out)) return LETHE_ERR_INVALID;
+  if (isnan(softmax_scale) || isinf(softmax_scale)) return LETHE_ERR_INVALID;
+  const size_t need = lethe_prefill_workspace_bytes(c, q_rows);
+  if (need > 0 && (!ws || ws_bytes < need)) return LETHE_ERR_WORKSPACE;
+  st = flush_pending(c, stream);
+  if (st != LETHE_OK) return st;
+  const int D = c->head_dim;
+  const int G = c->num_q_heads / c->num_kv_heads;
+  const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)D);
+  const size_t rowb = (size_t)D * 2;
+  const size_t lrow = (size_t)layer * (size_t)c->rows_per_layer;
+  PrefillArgs a;
+  a.k = (const char*)c->k + lrow * rowb;
+  a.v = (const char*)c->v + lrow * rowb;
+  a.score = c->score + lrow;
+  a.len = c->len;
+  a.seq_base = c->seq_base;
+  a.cap = c->cap;
+  a.rows_per_layer = c->rows_per_layer;
+  a.layer = layer;
+  a.B = c->num_seqs;
+  a.HK = c->num_kv_heads;
+  a.q = q;
+  a.q_start = q_start;
+  a.q_len = q_len;
+  a.q_rows = q_rows;
+  a.max_q = max_q_len;
+  a.max_kv = max_kv_len;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.out = out;
+  a.stat = (float*)ws;
+  a.dev_status = c->dev_status;
+  if (max_q_len == 0) return LETHE_OK;
+  return launch_prefill(a, D, G, stream);
+}
+
 lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* ws, size_t ws_bytes,
                               hipStream_t stream) {
   lethe_status st = check_cache(c);

@@ -150,6 +150,28 @@ struct SparsityArgs {
 
 lethe_status launch_sparsity(const SparsityArgs& a, hipStream_t s);
 
+struct PrefillArgs {
+  const void* k;          // the layer's first row
+  const void* v;
+  float* score;           // the layer's first row
+  const int32_t* len;     // [L][B]
+  const int64_t* seq_base;
+  const int32_t* cap;
+  int64_t rows_per_layer;
+  int32_t layer, B, HK;
+  const void* q;          // [q_rows][H_Q][D]
+  const int64_t* q_start; // [B]
+  const int32_t* q_len;   // [B]
+  int64_t q_rows;
+  int32_t max_q, max_kv;
+  float scale_log2;       // softmax scale * log2(e)
+  float* out;             // fp32 [q_rows][H_Q][D]
+  float* stat;            // fp32 [q_rows][H_Q][2]: max (base 2), 1 / sum
+  int32_t* dev_status;
+};
+
+lethe_status launch_prefill(const PrefillArgs& a, int D, int G, hipStream_t s);
+
 // Selection rules of launch_select.
 enum SelectMode : int32_t {
   kSelectRasr = 0,        // RASR per (layer, sequence, KV head)

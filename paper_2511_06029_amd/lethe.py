@@ -21,7 +21,7 @@ SHRINK_NO_BREAKPOINT, SHRINK_NOT_TRIGGERED = -1, -2
 EXPORTED = ("lethe_workspace_bytes", "lethe_state_bytes", "lethe_decode_attn_score",
             "lethe_layer_sparsity", "lethe_rasr_select", "lethe_rasr_select_shared",
             "lethe_segmented_shrink", "lethe_kv_compact", "lethe_score_flush",
-            "lethe_status_string")
+            "lethe_prefill_attn_score", "lethe_prefill_workspace_bytes", "lethe_status_string")
 
 
 class CCache(ctypes.Structure):
@@ -71,6 +71,11 @@ def load():
         lib.lethe_rasr_select_shared.restype = ctypes.c_int
         lib.lethe_segmented_shrink.argtypes = [pc, i32, ctypes.c_float, i32, i32, vp, vp, vp, vp, sz, vp]
         lib.lethe_segmented_shrink.restype = ctypes.c_int
+        lib.lethe_prefill_attn_score.argtypes = [pc, i32, vp, vp, vp, ctypes.c_int64, i32, i32, ctypes.c_float,
+                                                 vp, vp, sz, vp]
+        lib.lethe_prefill_attn_score.restype = ctypes.c_int
+        lib.lethe_prefill_workspace_bytes.argtypes = [pc, ctypes.c_int64]
+        lib.lethe_prefill_workspace_bytes.restype = sz
         lib.lethe_kv_compact.argtypes = [pc, vp, vp, sz, vp]
         lib.lethe_kv_compact.restype = ctypes.c_int
         lib.lethe_status_string.argtypes = [ctypes.c_int]
@@ -140,6 +145,19 @@ def rasr_select(cache, budget, recent, sink, keep, ws=None, stream=None):
     st = load().lethe_rasr_select(ctypes.byref(cache.c_struct()), _p(budget), int(recent), int(sink), _p(keep),
                                   _p(ws), nbytes, _stream(stream))
     _check("lethe_rasr_select", st)
+
+
+def prefill_attn_score(cache, layer, q, q_start, q_len, max_q_len, max_kv_len, softmax_scale, out, ws,
+                       stream=None):
+    """lethe_prefill_attn_score: causal prefill attention over the q_len newest
+    rows of every sequence, seeding their scores (Eq. 2).  q: bf16 [rows][H_Q][D];
+    q_start int64 [B], q_len int32 [B] (device); out fp32 like q."""
+    rows = q.shape[0]
+    st = load().lethe_prefill_attn_score(ctypes.byref(cache.c_struct()), int(layer), _p(q), _p(q_start), _p(q_len),
+                                         int(rows), int(max_q_len), int(max_kv_len), float(softmax_scale), _p(out),
+                                         _p(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                                         _stream(stream))
+    _check("lethe_prefill_attn_score", st)
 
 
 def rasr_select_shared(cache, budget, recent, sink, keep, ws=None, stream=None):
@@ -231,6 +249,10 @@ class LetheCache:
 
     def workspace(self, op):
         n = workspace_bytes(self, op)
+        return self.torch.zeros(max(n, 1), dtype=self.torch.uint8, device=self.k.device)
+
+    def prefill_workspace(self, q_rows):
+        n = int(load().lethe_prefill_workspace_bytes(ctypes.byref(self.c_struct()), int(q_rows)))
         return self.torch.zeros(max(n, 1), dtype=self.torch.uint8, device=self.k.device)
 
     def default_scale(self):

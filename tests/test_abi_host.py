@@ -138,6 +138,40 @@ def test_prune_argument_validation():
     assert lib.lethe_kv_compact(cc, FAKE, FAKE, need - 1, None) == L.ERR_WORKSPACE
 
 
+def test_prefill_validation_and_workspace():
+    lib = L.load()
+    c = make()
+    cc = ctypes.byref(c)
+    rows = 100
+    need = lib.lethe_prefill_workspace_bytes(cc, rows)
+    assert need >= rows * 32 * 2 * 4 and need % 256 == 0
+    assert lib.lethe_prefill_workspace_bytes(cc, 0) == 0
+    assert lib.lethe_prefill_workspace_bytes(cc, -1) == 0
+    assert lib.lethe_prefill_workspace_bytes(None, 5) == 0
+    pf = lib.lethe_prefill_attn_score
+
+    def call(layer=0, q=FAKE, qs=FAKE, ql=FAKE, rows=rows, mq=64, mkv=64, scale=0.0, out=FAKE, ws=FAKE, wsb=need,
+             cache=cc):
+        return pf(cache, layer, q, qs, ql, rows, mq, mkv, scale, out, ws, wsb, None)
+
+    assert call(layer=-1) == L.ERR_INVALID
+    assert call(layer=2) == L.ERR_INVALID
+    assert call(qs=None) == L.ERR_INVALID
+    assert call(ql=None) == L.ERR_INVALID
+    assert call(q=None) == L.ERR_INVALID
+    assert call(out=None) == L.ERR_INVALID
+    assert call(rows=-1) == L.ERR_INVALID
+    assert call(mq=-1) == L.ERR_INVALID
+    assert call(mkv=-1) == L.ERR_INVALID
+    for sc in (math.nan, math.inf):
+        assert call(scale=sc) == L.ERR_INVALID
+    assert call(ws=None) == L.ERR_WORKSPACE
+    assert call(wsb=need - 1) == L.ERR_WORKSPACE
+    assert call(cache=ctypes.byref(make(dtype=L.F32))) == L.ERR_UNSUPPORTED
+    assert call(cache=ctypes.byref(make(head_dim=96))) == L.ERR_UNSUPPORTED
+    assert call(cache=ctypes.byref(make(state=None))) == L.ERR_INVALID
+
+
 def test_state_sizes():
     lib = L.load()
     G, B, HQ, HK, D, Ly = 4, 4, 32, 8, 128, 2
