@@ -27,6 +27,11 @@ Prune rounds (--policy):
                 uniform layer budgets; sinks plus a window filling the
                 budget; PyramidKV's static layer budgets.  Same 40% budget.
 
+With --prefill the line instead measures lethe_prefill_attn_score on the
+same model shapes: one step is the causal prefill attention with score
+seeding (Eq. 2) of a 2048-token prompt for the 8 sequences, over all 32
+layers; the roofline is the matrix-core bf16 peak.
+
 The JSON line reports KV tokens scanned per second (one token = one cached
 (layer, sequence, position) row, all KV heads) over the whole timed run, the
 per-step decode latency, the prune-round latency, the HBM roofline of the
@@ -65,6 +70,7 @@ def parse():
                     default="lethe")
     ap.add_argument("--segments", type=int, default=10, help="Algorithm 1 segments D (shrink)")
     ap.add_argument("--tau", type=float, default=400.0, help="Algorithm 1 ratio threshold (shrink)")
+    ap.add_argument("--prefill", action="store_true", help="time the prompt prefill with score seeding instead")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="first copy MIB MiB device-to-device 3 times (counter calibration runs)")
     return ap.parse_args()
@@ -75,6 +81,10 @@ def main():
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+
+    if args.prefill:
+        run_prefill(args)
+        return
 
     import numpy as np
     import torch
@@ -270,6 +280,154 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cache, args.cpu_seconds, gamma, log)
     print(json.dumps(result), flush=True)
+
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def run_prefill(args):
+    """Prompt prefill with score seeding on the Llama-3-8B shapes, batch 8,
+    2048-token prompts, all 32 layers per step."""
+    import numpy as np
+    import torch
+
+    from paper_2511_06029_amd import lethe as L
+    from workloads import CONFIGS
+    from workloads.synth import ZipfCache
+
+    def log(msg):
+        print("[bench] " + msg, file=sys.stderr, flush=True)
+
+    cfg = CONFIGS[2]
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    Lyr, B, HQ, HK, D, T = cfg.num_layers, cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.prompt
+    log("allocating cache: %d layers x %d seqs x %d kv heads x %d rows" % (Lyr, B, HK, T))
+    cache = L.LetheCache(Lyr, [T] * B, HQ, HK, D, dtype="bf16", device=dev)
+    gen = ZipfCache(2, device=dev)
+    for l in range(Lyr):
+        for b in range(B):
+            K, V = gen.segment(l, b, T, T=T)
+            for h in range(HK):
+                s0, _ = cache.seg_rows(b, h)
+                cache.k[l, s0:s0 + T] = K[h]
+                cache.v[l, s0:s0 + T] = V[h]
+    cache.len.fill_(T)
+    rows = B * T
+    g = torch.Generator(device=dev)
+    g.manual_seed(2)
+    q = (torch.randn((Lyr, rows, HQ, D), generator=g, device=dev) * 1.0).to(torch.bfloat16)
+    q_start = torch.arange(B, dtype=torch.int64, device=dev) * T
+    q_len = torch.full((B,), T, dtype=torch.int32, device=dev)
+    out = torch.empty((rows, HQ, D), dtype=torch.float32, device=dev)
+    ws = cache.prefill_workspace(rows)
+    lib = L.load()
+    cref = ctypes.byref(cache.c_struct())
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    qp = [ctypes.c_void_p(q[l].data_ptr()) for l in range(Lyr)]
+    out_p, ws_p, wsb = ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel()
+    qs_p, ql_p = ctypes.c_void_p(q_start.data_ptr()), ctypes.c_void_p(q_len.data_ptr())
+    fn = lib.lethe_prefill_attn_score
+    torch.cuda.synchronize()
+
+    def step():
+        cache.score.zero_()
+        for l in range(Lyr):
+            rc = fn(cref, l, qp[l], qs_p, ql_p, rows, T, T, 0.0, out_p, ws_p, wsb, sp)
+            if rc != 0:
+                raise RuntimeError("lethe_prefill_attn_score: %s" % L.status_string(rc))
+
+    log("warm-up: %d step(s)" % args.warmup)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    log("timed: %d step(s)" % args.steps)
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        cache.score.zero_()
+        ev[k][0].record(stream)
+        for l in range(Lyr):
+            rc = fn(cref, l, qp[l], qs_p, ql_p, rows, T, T, 0.0, out_p, ws_p, wsb, sp)
+            if rc != 0:
+                raise RuntimeError("lethe_prefill_attn_score: %s" % L.status_string(rc))
+        ev[k][1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    status = int(cache.dev_status[0])
+    if status != 0:
+        raise RuntimeError("device status bits set: %d" % status)
+    elapsed = t1 - t0
+    call_ms = float(np.sum([e[0].elapsed_time(e[1]) for e in ev])) / (args.steps * Lyr)
+    # Algorithmic work of one call: causal Q K^T and P V once per query head,
+    # 4 D flops per (query, attended row) pair.
+    pairs = T * (T + 1) // 2
+    flops = 4.0 * D * pairs * B * HQ
+    achieved = flops / (call_ms / 1e3) / 1e12
+    tokens = B * T * args.steps
+    result = {
+        "metric": "prompt tokens/s (prefill attention + Eq. 2 score seeding, all layers)",
+        "value": tokens / elapsed,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Zipf key-bias caches, random queries)",
+        "config": {
+            "workload": "llama3-8b-shapes batch 8, 2048-token prompts, prefill with score seeding",
+            "layers": Lyr, "q_heads": HQ, "kv_heads": HK, "head_dim": D, "batch": B, "storage": "bf16",
+            "prompt": T,
+        },
+        "prefill_call_ms": call_ms,
+        "roofline": {
+            "bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+            "kernel": "prefill_fwd_kernel<128, 4> + prefill_score_kernel<128, 4> (lethe_prefill_attn_score, "
+                      "one call per layer)",
+            "flops_per_launch": flops, "launches": args.steps * Lyr,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = prefill_cpu_baseline(cache, q, args.cpu_seconds, log)
+    print(json.dumps(result), flush=True)
+
+
+def prefill_cpu_baseline(cache, q, budget_s, log):
+    """The oracle's prefill on whole (layer 0, sequence, KV head) segments for
+    about budget_s seconds of one host thread; a token is one prompt position
+    through one layer with all its heads."""
+    import numpy as np
+
+    import oracle
+
+    log("cpu baseline: oracle prefill on full-prompt segments (%.0f s budget)" % budget_s)
+    T = int(cache.len[0, 0])
+    G, D = cache.G, cache.D
+    qh = q[0].float().cpu().numpy()
+    segs, t_cpu = 0, 0.0
+    for b in range(cache.B):
+        for h in range(cache.HK):
+            s0, _ = cache.seg_rows(b, h)
+            K = cache.k[0, s0:s0 + T].float().cpu().numpy()
+            V = cache.v[0, s0:s0 + T].float().cpu().numpy()
+            t = time.perf_counter()
+            oracle.prefill(qh[b * T:(b + 1) * T, h * G:(h + 1) * G], K, V, None, 1 / math.sqrt(D))
+            t_cpu += time.perf_counter() - t
+            segs += 1
+            if t_cpu >= budget_s:
+                break
+        if t_cpu >= budget_s:
+            break
+    tokens = segs * T / cache.HK
+    return {"value": tokens / t_cpu, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": "oracle prefill attention + score seeding of %d (layer 0, seq, kv-head) segments of %d "
+                      "prompt tokens (%.1f s on one host thread)" % (segs, T, t_cpu)}
 
 
 def kernel_source_hash():
