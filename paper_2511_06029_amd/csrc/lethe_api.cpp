@@ -275,8 +275,9 @@ lethe_status lethe_segmented_shrink(const lethe_cache* c, int32_t segments, floa
 }
 
 size_t lethe_prefill_workspace_bytes(const lethe_cache* c, int64_t q_rows) {
-  if (!c || q_rows < 0 || c->num_q_heads <= 0) return 0;
-  return align_up((size_t)q_rows * (size_t)c->num_q_heads * 2 * sizeof(float), 256);
+  if (!c || q_rows <= 0 || c->num_q_heads <= 0) return 0;
+  // (max, 1 / sum) per query row and head, plus slack for reads in pairs.
+  return align_up((size_t)q_rows * (size_t)c->num_q_heads * 2 * sizeof(float) + 16, 256);
 }
 
 lethe_status lethe_prefill_attn_score(const lethe_cache* c, int32_t layer, const void* q,

@@ -62,6 +62,52 @@ struct PfCfg {
   static constexpr int BUF = KTILE + VTILE;
 };
 
+// s_waitcnt with only a vector-memory count (expcnt and lgkmcnt left free).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Transposing 64-bit LDS read of four bf16 values.  Written as inline
+// assembly so that the compiler does not order it after every outstanding
+// direct-to-LDS load (it cannot tell which buffer those fill).  The compiler
+// does not track these reads either: lgkm_fence() must run before the
+// results are used.
+__device__ inline pf_bf16x4_t lds_read_tr(const pf_lds_char_t* p) {
+  typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+  u32x2_t r;
+  const unsigned addr = (unsigned)(unsigned long)p;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(addr));
+  return __builtin_bit_cast(pf_bf16x4_t, r);
+}
+
+// Waits for every outstanding LDS read.  The operands tie the wait to the
+// registers those reads fill, so no use of them can be scheduled before it.
+template <int NT>
+__device__ inline void lgkm_fence(pf_bf16x8_t (&v)[NT]) {
+  static_assert(NT == 4 || NT == 8, "operand tiles");
+  if constexpr (NT == 4) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
+  } else {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7]));
+  }
+}
+
+// 64-bit LDS read that waits for its own result (same reason as lds_read_tr).
+__device__ inline float2 lds_read_f2(const pf_lds_char_t* p) {
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  f32x2_t r;
+  const unsigned addr = (unsigned)(unsigned long)p;
+  asm volatile("ds_read_b64 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(addr));
+  return make_float2(r[0], r[1]);
+}
+
+// 2^x by the hardware instruction alone (results below 2^-126 flush to 0,
+// which softmax weights never need; 2^-inf = 0).
+__device__ inline float pf_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ inline pf_bf16x8_t pf_zero8() {
   pf_bf16x8_t z;
 #pragma unroll
@@ -99,7 +145,11 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2)))
   using Cfg = PfCfg<D>;
   constexpr int KK = Cfg::KK, NT = Cfg::NT, ROWB = Cfg::ROWB, CH = Cfg::CH;
   constexpr int NQUAD = (G + 3) / 4;
-  __shared__ __attribute__((aligned(16))) char tiles[2][Cfg::BUF];
+  constexpr int NBUF = 3;  // tiles st, st + 1 and st + 2 in flight
+  constexpr int KLOADS = Cfg::KTILE / (kWave * 16);
+  constexpr int LPW = (KLOADS + Cfg::VLOADS) / kPfWaves;  // direct loads per wave and step
+  static_assert((KLOADS + Cfg::VLOADS) % kPfWaves == 0, "loads split evenly over the waves");
+  __shared__ __attribute__((aligned(16))) char tiles[NBUF][Cfg::BUF];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -146,7 +196,7 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2)))
     const int j0 = st * Cfg::STEP;
     char* kt = tiles[buf];
     char* vt = tiles[buf] + Cfg::KTILE;
-    constexpr int KLOADS = Cfg::KTILE / (kWave * 16);
+#pragma unroll
     for (int t = w; t < KLOADS + Cfg::VLOADS; t += kPfWaves) {
       if (t < KLOADS) {
         const int q = kWave * t + lane;
@@ -169,31 +219,32 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2)))
   for (int nt = 0; nt < NT; ++nt) o[nt][0] = o[nt][1] = pf_f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
   issue(0, 0);
+  if (nsteps > 1) issue(1, 1);
   const int rsub = 4 * g4 + (s >> 2);
   for (int st = 0; st < nsteps; ++st) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();  // tile st landed for every wave; tile st - 1 fully read
-    const int j0 = st * Cfg::STEP;
-    const char* kt = tiles[st & 1];
-    pf_lds_char_t* vt = (pf_lds_char_t*)(tiles[st & 1] + Cfg::KTILE);
-    // V^T operands first, through the transposing LDS read (lane s of group
-    // g4 points at row 4 g4 + s / 4 and 16 rows further, column
-    // 16 nt + 4 (s mod 4)): the compiler orders these reads after every
-    // outstanding direct load, so they go before the next tile is requested.
-    pf_bf16x8_t av[NT];
-    if (active) {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int col = (16 * nt + 4 * (s & 3)) * 2;
-        const pf_bf16x4_t a0 =
-            __builtin_amdgcn_ds_read_tr16_b64_v4bf16(reinterpret_cast<pf_lds_bf16x4_t*>(vt + Cfg::vaddr(rsub, col)));
-        const pf_bf16x4_t a1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            reinterpret_cast<pf_lds_bf16x4_t*>(vt + Cfg::vaddr(rsub + 16, col)));
-        av[nt] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-      }
-    }
-    if (st + 1 < nsteps) issue(st + 1, (st + 1) & 1);
+    // This wave's loads of tile st are done once at most the LPW loads of
+    // tile st + 1 are outstanding; the barrier makes every wave's visible
+    // and guarantees tile st - 1 has been read by all.
+    if (st + 1 < nsteps)
+      wait_vmcnt<LPW>();
+    else
+      wait_vmcnt<0>();
+    __syncthreads();
+    if (st + 2 < nsteps) issue(st + 2, (st + 2) % NBUF);
     if (!active) continue;
+    const int j0 = st * Cfg::STEP;
+    const char* kt = tiles[st % NBUF];
+    const pf_lds_char_t* vt = (const pf_lds_char_t*)(tiles[st % NBUF] + Cfg::KTILE);
+    // V^T operands through the transposing LDS read: lane s of group g4
+    // points at row 4 g4 + s / 4 and 16 rows further, column 16 nt + 4 (s mod 4).
+    pf_bf16x8_t av[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int col = (16 * nt + 4 * (s & 3)) * 2;
+      const pf_bf16x4_t a0 = lds_read_tr(vt + Cfg::vaddr(rsub, col));
+      const pf_bf16x4_t a1 = lds_read_tr(vt + Cfg::vaddr(rsub + 16, col));
+      av[nt] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
 
     pf_f32x4_t sacc[2][2];
 #pragma unroll
@@ -211,27 +262,38 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2)))
       }
     }
 
-    // Softmax of query 16 qt + s over keys j0 + 16 T + 4 g4 + rr.
+    // Softmax of query 16 qt + s over keys j0 + 16 T + 4 g4 + rr.  Steps
+    // wholly below the diagonal (every key precedes every query of the tile
+    // and is live) skip the mask.
+    const bool interior = j0 + Cfg::STEP - 1 <= p0 && j0 + Cfg::STEP <= kend;
     pf_bf16x8_t ph[2], pl[2];
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
       const int pos = p0 + 16 * qt + s;
       float x[8];
       float mx = kPfNegBig;
+      if (interior) {
 #pragma unroll
-      for (int jj = 0; jj < 8; ++jj) {
-        const int key = j0 + 16 * (jj >> 2) + 4 * g4 + (jj & 3);
-        x[jj] = (key <= pos && key < kend) ? sacc[jj >> 2][qt][jj & 3] * sc : -INFINITY;
-        mx = fmaxf(mx, x[jj]);
+        for (int jj = 0; jj < 8; ++jj) {
+          x[jj] = sacc[jj >> 2][qt][jj & 3] * sc;
+          mx = fmaxf(mx, x[jj]);
+        }
+      } else {
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const int key = j0 + 16 * (jj >> 2) + 4 * g4 + (jj & 3);
+          x[jj] = (key <= pos && key < kend) ? sacc[jj >> 2][qt][jj & 3] * sc : -INFINITY;
+          mx = fmaxf(mx, x[jj]);
+        }
       }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float mnew = fmaxf(m[qt], mx);
-      const float corr = exp2f(m[qt] - mnew);
+      const float corr = pf_exp2(m[qt] - mnew);
       float psum = 0.0f;
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) {
-        const float p = exp2f(x[jj] - mnew);
+        const float p = pf_exp2(x[jj] - mnew);
         psum += p;
         const __bf16 hi = (__bf16)p;
         ph[qt][jj] = hi;
@@ -239,11 +301,16 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2)))
       }
       l[qt] = l[qt] * corr + psum;
       m[qt] = mnew;
+      // Once the running maxima settle most steps leave every lane's
+      // correction at exactly 1; the wave then skips the rescale.
+      if (__any(corr != 1.0f)) {
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) o[nt][qt] *= corr;
+        for (int nt = 0; nt < NT; ++nt) o[nt][qt] *= corr;
+      }
     }
 
     // O^T += V^T P^T.
+    lgkm_fence<NT>(av);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
 #pragma unroll
@@ -271,7 +338,8 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2)))
       const pf_f32x4_t v = o[nt][qt] * inv;
       *reinterpret_cast<float4*>(orow + 16 * nt + 4 * g4) = make_float4(v[0], v[1], v[2], v[3]);
     }
-    if (g4 == 0) *reinterpret_cast<float2*>(a.stat + 2 * qrow) = make_float2(m[qt], inv);
+    if (g4 == 0)
+      *reinterpret_cast<float2*>(a.stat + 2 * ((long long)(h * G + g) * a.q_rows + sq.q0 + i)) = make_float2(m[qt], inv);
   }
 }
 
@@ -280,13 +348,20 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2)))
 // ---------------------------------------------------------------------------
 constexpr int kPfKeysPerWave = 64;
 constexpr int kPfKeysPerBlock = kPfWaves * kPfKeysPerWave;
+constexpr int kPfItemQ = 32;  // queries of one head per work item
 
 template <int D, int G>
 __global__ __launch_bounds__(kPfThreads) void prefill_score_kernel(PrefillArgs a) {
   using Cfg = PfCfg<D>;
   constexpr int KK = Cfg::KK, ROWB = Cfg::ROWB, CH = Cfg::CH;
-  constexpr int QTILE = 16 * ROWB;  // 16 query rows of one head
-  __shared__ __attribute__((aligned(16))) char qtiles[2][QTILE];
+  constexpr int QTILE = kPfItemQ * ROWB;
+  constexpr int STATB = kPfItemQ * 8;  // (max, 1 / sum) per query
+  constexpr int BUFB = QTILE + STATB;
+  constexpr int NBUF = 3;
+  constexpr int QLOADS = QTILE / (kWave * 16);
+  static_assert(QLOADS % kPfWaves == 0, "query loads split evenly over the waves");
+  constexpr int LPW = QLOADS / kPfWaves;  // plus one statistics load on wave 0
+  __shared__ __attribute__((aligned(16))) char bufs[NBUF][BUFB];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -315,21 +390,30 @@ __global__ __launch_bounds__(kPfThreads) void prefill_score_kernel(PrefillArgs a
       kr[T][kk] = *reinterpret_cast<const pf_bf16x8_t*>(Kb + (long long)row * ROWB + 64 * kk + 16 * g4);
   }
 
-  // Work items: (query tile of 16, head) for every tile holding a position
+  // Work items: (tile of 32 queries, head) for every tile holding a position
   // at or after the block's first key.
-  const int it0 = max(0, kblk0 - sq.first) / 16;
-  const int nit = (sq.qlen + 15) / 16 - it0;
+  const int it0 = max(0, kblk0 - sq.first) / kPfItemQ;
+  const int nit = (sq.qlen + kPfItemQ - 1) / kPfItemQ - it0;
   const int nitems = nit * G;
   auto issue = [&](int item, int buf) {
     const int it = it0 + item / G, g = item % G;
-    constexpr int LOADS = QTILE / (kWave * 16);
-    for (int t = w; t < LOADS; t += kPfWaves) {
+#pragma unroll
+    for (int t = w; t < QLOADS; t += kPfWaves) {
       const int q = kWave * t + lane;
       const int r = q / CH, c = (q % CH) ^ (r % CH);
-      const int i = min(16 * it + r, sq.qlen - 1);
+      const int i = min(kPfItemQ * it + r, sq.qlen - 1);
       const char* src = reinterpret_cast<const char*>(a.q) + ((sq.q0 + i) * HQ + (long long)h * G + g) * ROWB + 16 * c;
       __builtin_amdgcn_global_load_lds((pf_global_cvoid_t*)src,
-                                       (pf_lds_void_t*)((pf_lds_char_t*)qtiles[buf] + kWave * 16 * t), 16, 0, 0);
+                                       (pf_lds_void_t*)((pf_lds_char_t*)bufs[buf] + kWave * 16 * t), 16, 0, 0);
+    }
+    if (w == 0 && lane < kPfItemQ / 2) {
+      // Statistics of the item's queries: 32 x 8 bytes, two queries a lane.
+      // A pair may reach one entry past the live ones (the workspace has
+      // slack for it); those entries belong to masked queries.
+      const int i = min(kPfItemQ * it + 2 * lane, sq.qlen - 1);
+      const float* src = a.stat + 2 * ((long long)(h * G + g) * a.q_rows + sq.q0 + i);
+      __builtin_amdgcn_global_load_lds((pf_global_cvoid_t*)src, (pf_lds_void_t*)((pf_lds_char_t*)bufs[buf] + QTILE),
+                                       16, 0, 0);
     }
   };
 
@@ -340,37 +424,55 @@ __global__ __launch_bounds__(kPfThreads) void prefill_score_kernel(PrefillArgs a
     for (int rr = 0; rr < 4; ++rr) acc[T][rr] = 0.0f;
 
   if (nitems > 0) issue(0, 0);
+  if (nitems > 1) issue(1, 1);
   for (int item = 0; item < nitems; ++item) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (item + 1 < nitems) issue(item + 1, (item + 1) & 1);
-    const int it = it0 + item / G, g = item % G;
-    // Skip when every query of the tile precedes this wave's keys.
-    if (sq.first + 16 * it + 15 < j0w || j0w >= sq.n) continue;
-    const char* qt = qtiles[item & 1];
-    pf_bf16x8_t qv[KK];
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-      qv[kk] = *reinterpret_cast<const pf_bf16x8_t*>(qt + 16 * Cfg::kslot(s, 4 * kk + g4));
-    const int i = 16 * it + s;
-    const bool valid = i < sq.qlen;
-    float mq = 0.0f, iq = 0.0f;
-    if (valid) {
-      const float2 st = *reinterpret_cast<const float2*>(a.stat + 2 * ((sq.q0 + i) * HQ + (long long)h * G + g));
-      mq = st.x;
-      iq = st.y;
+    if (item + 1 < nitems) {
+      if (w == 0)
+        wait_vmcnt<LPW + 1>();
+      else
+        wait_vmcnt<LPW>();
+    } else {
+      wait_vmcnt<0>();
     }
-    const int pos = sq.first + i;
+    __syncthreads();
+    if (item + 2 < nitems) issue(item + 2, (item + 2) % NBUF);
+    const int it = it0 + item / G;
+    const int pos0 = sq.first + kPfItemQ * it;  // position of the tile's first query
+    // Nothing to do when every query of the tile precedes this wave's keys.
+    if (pos0 + kPfItemQ - 1 < j0w || j0w >= sq.n) continue;
+    const char* qt = bufs[item % NBUF];
+    const float* stl = reinterpret_cast<const float*>(qt + QTILE);
+    // No masking when every key is live and precedes every (live) query.
+    const bool full = j0w + kPfKeysPerWave - 1 <= pos0 && kPfItemQ * (it + 1) <= sq.qlen &&
+                      j0w + kPfKeysPerWave <= sq.n;
 #pragma unroll
-    for (int T = 0; T < 4; ++T) {
-      pf_f32x4_t sacc = pf_f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int qh = 0; qh < kPfItemQ / 16; ++qh) {
+      pf_bf16x8_t qv[KK];
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], qv[kk], sacc, 0, 0, 0);
+      for (int kk = 0; kk < KK; ++kk)
+        qv[kk] = *reinterpret_cast<const pf_bf16x8_t*>(qt + 16 * Cfg::kslot(16 * qh + s, 4 * kk + g4));
+      // exp2(x - max) / sum = exp2(x - (max + log2(sum))).
+      const float2 st = lds_read_f2((const pf_lds_char_t*)(stl + 2 * (16 * qh + s)));
+      const float off = st.x - __log2f(st.y);
+      const int i = kPfItemQ * it + 16 * qh + s;
+      const int pos = sq.first + i;
+      const bool valid = i < sq.qlen;
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int key = j0w + 16 * T + 4 * g4 + rr;
-        const float p = exp2f(sacc[rr] * sc - mq) * iq;
-        acc[T][rr] += (valid && key <= pos && key < sq.n) ? p : 0.0f;
+      for (int T = 0; T < 4; ++T) {
+        pf_f32x4_t sacc = pf_f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], qv[kk], sacc, 0, 0, 0);
+        if (full) {
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) acc[T][rr] += pf_exp2(fmaf(sacc[rr], sc, -off));
+        } else {
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int key = j0w + 16 * T + 4 * g4 + rr;
+            const float p = pf_exp2(fmaf(sacc[rr], sc, -off));
+            acc[T][rr] += (valid && key <= pos && key < sq.n) ? p : 0.0f;
+          }
+        }
       }
     }
   }
