@@ -129,7 +129,7 @@ __device__ void write_partial(const CombineLds& cb, float* part) {
     float lsum = 0.0f, o0 = 0.0f, o1 = 0.0f;
 #pragma unroll
     for (int k = 0; k < kNumWaves; ++k) {
-      const float f = exp2f(cb.m[k][g] - mx);
+      const float f = hw_exp2(cb.m[k][g] - mx);
       lsum += cb.l[k][g] * f;
       o0 += cb.o[k][g][d] * f;
       o1 += cb.o[k][g][d + 1] * f;
@@ -155,7 +155,7 @@ __device__ void finish_single(const DecodeArgs& a, const Chunk& ck, const Combin
     float lsum = 0.0f, o0 = 0.0f, o1 = 0.0f;
 #pragma unroll
     for (int k = 0; k < kNumWaves; ++k) {
-      const float f = exp2f(cb.m[k][g] - mx);
+      const float f = hw_exp2(cb.m[k][g] - mx);
       lsum += cb.l[k][g] * f;
       o0 += cb.o[k][g][d] * f;
       o1 += cb.o[k][g][d + 1] * f;
@@ -193,13 +193,13 @@ __device__ void combine_segment(const DecodeArgs& a, const Chunk& ck, int nne) {
       float bm = M;
 #pragma unroll
       for (int k = 0; k < NB; ++k) bm = (c0 + k < nne) ? fmaxf(bm, ml[k].x) : bm;
-      const float f = exp2f(M - bm);
+      const float f = hw_exp2(M - bm);
       lsum *= f;
       o0 *= f;
       o1 *= f;
 #pragma unroll
       for (int k = 0; k < NB; ++k) {
-        const float wgt = (c0 + k < nne) ? exp2f(ml[k].x - bm) : 0.0f;
+        const float wgt = (c0 + k < nne) ? hw_exp2(ml[k].x - bm) : 0.0f;
         lsum = fmaf(ml[k].y, wgt, lsum);
         o0 = fmaf(ov[k].x, wgt, o0);
         o1 = fmaf(ov[k].y, wgt, o1);
@@ -361,7 +361,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
           so = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qo[kk], kr[T][kk], so, 0, 0, 0);
         float acc = 0.0f;
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) acc = fmaf(exp2f(fmaf(so[rr], pd.scale, -pm[rr])), pi[rr], acc);
+        for (int rr = 0; rr < 4; ++rr) acc = fmaf(hw_exp2(fmaf(so[rr], pd.scale, -pm[rr])), pi[rr], acc);
         part[T] = acc + __shfl_xor(acc, 16);
       }
       if (pon) pd.score[prow] = fmaf(pd.gamma, sold, g4 == 0 ? part[0] : part[1]);
@@ -383,12 +383,12 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float mnew = fmaxf(m, mx);
-    const float corr = exp2f(m - mnew);
+    const float corr = hw_exp2(m - mnew);
     float psum = 0.0f;
     bf16x8_t ph, pl;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const float p = exp2f(x[j >> 2][j & 3] - mnew);
+      const float p = hw_exp2(x[j >> 2][j & 3] - mnew);
       psum += p;
       const __bf16 hi = (__bf16)p;
       ph[j] = hi;
@@ -450,8 +450,8 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
     acc += __shfl_xor(acc, 32);
     const float x = acc * sc;
     const float mnew = fmaxf(m, x);
-    const float corr = exp2f(m - mnew);
-    const float p = exp2f(x - mnew);
+    const float corr = hw_exp2(m - mnew);
+    const float p = hw_exp2(x - mnew);
     l = l * corr + (g4 == 0 ? p : 0.0f);
     m = mnew;
     const uint16_t* vv = reinterpret_cast<const uint16_t*>(vn);
@@ -570,7 +570,7 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
 #pragma unroll
           for (int e = 0; e < EPL; ++e) acc = fmaf(qof[g][e], kf[e], acc);
           const float xs = group_sum<LPR>(acc);
-          c = fmaf(exp2f(xs - pM[g]), pI[g], c);
+          c = fmaf(hw_exp2(xs - pM[g]), pI[g], c);
         }
         if (dp == 0 && row[u] < pre_end) pd.score[row[u]] = fmaf(pd.gamma, sold[u], c);
       }
@@ -580,13 +580,13 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
       float mx = m[g];
 #pragma unroll
       for (int u = 0; u < U; ++u) mx = fmaxf(mx, x[u][g]);
-      const float corr = exp2f(m[g] - mx);
+      const float corr = hw_exp2(m[g] - mx);
       float lg = l[g] * corr;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) o[g][e] *= corr;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const float p = exp2f(x[u][g] - mx);
+        const float p = hw_exp2(x[u][g] - mx);
         float vf[EPL];
         Elem<float>::unpack(vr[u], vf);
         lg += p;
@@ -647,8 +647,8 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
       const float mo = __shfl_xor(m[g], off);
       const float lo = __shfl_xor(l[g], off);
       const float mx = fmaxf(m[g], mo);
-      const float fa = exp2f(m[g] - mx);
-      const float fb = exp2f(mo - mx);
+      const float fa = hw_exp2(m[g] - mx);
+      const float fb = hw_exp2(mo - mx);
       l[g] = l[g] * fa + lo * fb;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
@@ -884,7 +884,7 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
       float acc = 0.0f;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) acc = fmaf(qf[g][e], kf[e], acc);
-      c = fmaf(exp2f(group_sum<LPR>(acc) - M[g]), iL[g], c);
+      c = fmaf(hw_exp2(group_sum<LPR>(acc) - M[g]), iL[g], c);
     }
     if (dp == 0 && r < rows) score[r] = fmaf(gamma, score[r], c);
   }

@@ -78,6 +78,11 @@ __device__ inline float group_sum(float v) {
   return v;
 }
 
+// 2^x by the hardware instruction alone: results below 2^-126 flush to 0,
+// which softmax weights and their rescaling factors never need; 2^-inf = 0.
+// (The library exp2f adds a range fix-up of four more instructions.)
+__device__ inline float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ inline float wave_max(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
   return v;

@@ -104,10 +104,6 @@ __device__ inline float2 lds_read_f2(const pf_lds_char_t* p) {
   return make_float2(r[0], r[1]);
 }
 
-// 2^x by the hardware instruction alone (results below 2^-126 flush to 0,
-// which softmax weights never need; 2^-inf = 0).
-__device__ inline float pf_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
 __device__ inline pf_bf16x8_t pf_zero8() {
   pf_bf16x8_t z;
 #pragma unroll
@@ -289,11 +285,11 @@ __global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2)))
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float mnew = fmaxf(m[qt], mx);
-      const float corr = pf_exp2(m[qt] - mnew);
+      const float corr = hw_exp2(m[qt] - mnew);
       float psum = 0.0f;
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) {
-        const float p = pf_exp2(x[jj] - mnew);
+        const float p = hw_exp2(x[jj] - mnew);
         psum += p;
         const __bf16 hi = (__bf16)p;
         ph[qt][jj] = hi;
@@ -464,12 +460,12 @@ __global__ __launch_bounds__(kPfThreads) void prefill_score_kernel(PrefillArgs a
         for (int kk = 0; kk < KK; ++kk) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], qv[kk], sacc, 0, 0, 0);
         if (full) {
 #pragma unroll
-          for (int rr = 0; rr < 4; ++rr) acc[T][rr] += pf_exp2(fmaf(sacc[rr], sc, -off));
+          for (int rr = 0; rr < 4; ++rr) acc[T][rr] += hw_exp2(fmaf(sacc[rr], sc, -off));
         } else {
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
             const int key = j0w + 16 * T + 4 * g4 + rr;
-            const float p = pf_exp2(fmaf(sacc[rr], sc, -off));
+            const float p = hw_exp2(fmaf(sacc[rr], sc, -off));
             acc[T][rr] += (valid && key <= pos && key < sq.n) ? p : 0.0f;
           }
         }
