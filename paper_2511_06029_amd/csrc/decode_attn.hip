@@ -76,13 +76,18 @@ struct Chunk {
   bool app;          // a row is appended to this sequence
   long long segrow0; // first row of the segment in the layer
   int32_t* next;     // the segment's step counter
-  int first, stride; // fixed schedule: steps first, first + stride, ... (stride 0: counter)
+  int first, stride; // wave w's first step is first + w; then first + w + stride, ...
+                     // (stride 0: from the counter, whose n-th reply is step dyn_base + n)
+  int dyn_base;
 };
 
-// A wavefront's next step: from the segment's counter (whichever wave asks
-// first), or from the fixed schedule.  step_request issues the request (the
-// counter's reply lands in lane 0 of the returned register); step_index reads
-// it when it is needed, so the atomic's latency overlaps other work.
+// A wavefront's steps after its first (which is fixed, so its loads need no
+// round trip): from the segment's counter (whichever wave asks first), or
+// from the fixed schedule.  step_request issues the request (the counter's
+// reply lands in lane 0 of the returned register); step_index reads it when
+// it is needed, so the atomic's latency overlaps other work.  Every step
+// below the segment's count is held by one wave and each holder asks once
+// more, so exactly one wave receives the index equal to the count.
 __device__ inline int step_request(const Chunk& ck, int& fixed_next, int lane) {
   if (ck.stride) {
     const int v = fixed_next;
@@ -90,7 +95,7 @@ __device__ inline int step_request(const Chunk& ck, int& fixed_next, int lane) {
     return v;
   }
   int v = 0;
-  if (lane == 0) v = __hip_atomic_fetch_add(ck.next, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (lane == 0) v = ck.dyn_base + __hip_atomic_fetch_add(ck.next, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return v;
 }
 __device__ inline int step_index(int raw) { return __builtin_amdgcn_readfirstlane(raw); }
@@ -254,9 +259,9 @@ __device__ inline bf16x8_t q_operand(const char* qgroup, int s, int g4, int kk) 
                  : zero_bf16x8();
 }
 
-template <int D, int G>
-__device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pending<G>& pd, char* vtiles,
-                                CombineLds& cb) {
+template <int D, int G, class ReadPending>
+__device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const ReadPending& read_pending,
+                                char* vtiles, CombineLds& cb) {
   using Cfg = MfmaCfg<D>;
   constexpr int KK = Cfg::KK, NT = Cfg::NT, ROWB = Cfg::ROWB;
   constexpr int STEP = Cfg::STEP, LPR = Cfg::LPR, VLOADS = Cfg::VLOADS;
@@ -270,8 +275,47 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
   char* vb = vtiles + w * Cfg::TILE_BYTES;
 
   const int re = ck.ncache;
-  const int pre_end = min(pd.rows, re);
   const int nsteps = (re + STEP - 1) / STEP;
+  const char* Kb = reinterpret_cast<const char*>(a.k) + ck.segrow0 * ROWB;
+  const char* Vb = reinterpret_cast<const char*>(a.v) + ck.segrow0 * ROWB;
+  float* const sseg = a.score + ck.segrow0;
+
+  // Loads of a step: K rows into the operand registers and the old scores of
+  // rows base + 16 g4 + s (lane groups 0 and 1, used if the pending update
+  // covers them); V rows straight into the wave's LDS tile.  The next step's
+  // K and scores are requested as soon as this step's K has gone through the
+  // MFMAs, and its V as soon as this step's V^T reads have completed, so the
+  // loads of one step overlap the softmax and PV work of the previous one.
+  // The first step is fixed, so its loads leave before anything else is read.
+  bf16x8_t kr[2][KK];
+  float sold = 0.0f;
+  auto load_k = [&](int bs) {
+#pragma unroll
+    for (int T = 0; T < 2; ++T) {
+      const int row = min(bs + 16 * T + s, re - 1);
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        kr[T][kk] = *reinterpret_cast<const bf16x8_t*>(Kb + (long long)row * ROWB + 64 * kk + 16 * g4);
+    }
+    sold = g4 < 2 ? sseg[min(bs + 16 * g4 + s, re - 1)] : 0.0f;
+  };
+  auto load_v = [&](int bs) {
+#pragma unroll
+    for (int u = 0; u < VLOADS; ++u) {
+      const int row = min(bs + u + VLOADS * (lane / LPR), re - 1);
+      __builtin_amdgcn_global_load_lds((global_cvoid_t*)(Vb + (long long)row * ROWB + 16 * (lane % LPR)),
+                                       (lds_void_t*)((lds_char_t*)vb + u * Cfg::VBLK), 16, 0, 0);
+    }
+  };
+  int idx = ck.first + w;
+  int fixed_next = idx + ck.stride;
+  if (idx < nsteps) {
+    load_k(idx * STEP);
+    load_v(idx * STEP);
+  }
+
+  const Pending<G> pd = read_pending();
+  const int pre_end = min(pd.rows, re);
   // Both query sets live in registers; so do the pending step's statistics
   // of the heads 4 g4 + rr this lane holds in S = Q_prev K^T.
   const char* qcur = reinterpret_cast<const char*>(a.q) + ((long long)ck.b * HQ + (long long)ck.h * G) * D * 2;
@@ -295,46 +339,9 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-  const char* Kb = reinterpret_cast<const char*>(a.k) + ck.segrow0 * ROWB;
-  const char* Vb = reinterpret_cast<const char*>(a.v) + ck.segrow0 * ROWB;
   const float sc = a.scale_log2;
-
-  // Loads of a step: K rows into the operand registers and, for the pending
-  // update, the old scores of rows base + 16 g4 + s (lane groups 0 and 1);
-  // V rows straight into the wave's LDS tile.  The next step's K and scores
-  // are requested as soon as this step's K has gone through the MFMAs, and
-  // its V as soon as this step's V^T reads have completed, so the loads of
-  // one step overlap the softmax and PV work of the previous one.
-  bf16x8_t kr[2][KK];
-  float sold = 0.0f;
-  auto load_k = [&](int bs) {
-#pragma unroll
-    for (int T = 0; T < 2; ++T) {
-      const int row = min(bs + 16 * T + s, re - 1);
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        kr[T][kk] = *reinterpret_cast<const bf16x8_t*>(Kb + (long long)row * ROWB + 64 * kk + 16 * g4);
-    }
-    const int prow = bs + 16 * g4 + s;
-    sold = (g4 < 2 && prow < pre_end) ? pd.score[prow] : 0.0f;
-  };
-  auto load_v = [&](int bs) {
-#pragma unroll
-    for (int u = 0; u < VLOADS; ++u) {
-      const int row = min(bs + u + VLOADS * (lane / LPR), re - 1);
-      __builtin_amdgcn_global_load_lds((global_cvoid_t*)(Vb + (long long)row * ROWB + 16 * (lane % LPR)),
-                                       (lds_void_t*)((lds_char_t*)vb + u * Cfg::VBLK), 16, 0, 0);
-    }
-  };
-  int fixed_next = ck.first + w;
-  int graw = step_request(ck, fixed_next, lane);
-  int idx = step_index(graw);
   int nidx = nsteps + 1;
-  if (idx < nsteps) {
-    load_k(idx * STEP);
-    load_v(idx * STEP);
-    graw = step_request(ck, fixed_next, lane);
-  }
+  int graw = idx < nsteps ? step_request(ck, fixed_next, lane) : 0;
   while (idx < nsteps) {
     const int base = idx * STEP;
     nidx = step_index(graw);
@@ -484,8 +491,9 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Pend
 // ---------------------------------------------------------------------------
 // fp32 path (VALU): 16-byte loads, D/4 lanes per row.
 // ---------------------------------------------------------------------------
-template <int D, int G>
-__device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pending<G>& pd, CombineLds& cb) {
+template <int D, int G, class ReadPending>
+__device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const ReadPending& read_pending,
+                               CombineLds& cb) {
   constexpr int EPL = 4;
   constexpr int LPR = D / EPL;
   constexpr int RPW = kWave / LPR;
@@ -497,6 +505,7 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
   const int rg = lane / LPR;
   const int dp = lane % LPR;
   const int HQ = a.HK * G;
+  const Pending<G> pd = read_pending();
 
   // Queries pre-scaled by their step's scale, so both logit sums below are
   // formed the same way.
@@ -598,9 +607,9 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const Pendi
     }
   };
 
-  int fixed_next = ck.first + w;
+  int fixed_next = ck.first + w + ck.stride;
   auto grab = [&]() { return step_index(step_request(ck, fixed_next, lane)); };
-  int idx = grab();
+  int idx = ck.first + w;
   for (; idx < nsteps; idx = grab()) {
     const int base = idx * ROWS_WAVE;
     uint4 kr[U], vr[U];
@@ -724,7 +733,6 @@ __device__ inline void decode_body(const DecodeArgs& a) {
     }
     return;
   }
-  const int par = a.pend_par[b] & 1;
   const size_t qgroup = ((size_t)b * HQ + (size_t)h * G) * D * sizeof(T);  // bytes
   const size_t qhalf = (size_t)a.B * HQ * D * sizeof(T);
 
@@ -734,8 +742,9 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   ck.seg = seg;
   ck.c = c;
   ck.next = &a.seg_cnt[(long long)seg * kCntStride + kStepCounter];
-  ck.first = c * kNumWaves;  // fixed schedule: wave w starts at step c * waves + w
+  ck.first = c * kNumWaves;  // wave w starts at step c * waves + w
   ck.stride = a.deterministic ? a.nch * kNumWaves : 0;
+  ck.dyn_base = a.nch * kNumWaves;
   ck.app = app;
   ck.ncache = n;
   ck.segrow0 = sbase + (long long)h * cp;
@@ -746,14 +755,25 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   // block that finishes a segment later reads the count: all of them do so
   // after every block of its segment has counted, so the last segment to
   // finish sees the full count and publishes the new length and pending
-  // step; earlier finishers that also see it publish the same values.
-  const int pend_rows = a.pend_len[b];
-  const float pend_gamma = a.pend_gamma[b];
-  const float pend_scale = a.pend_scale[b];
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  // step; earlier finishers that also see it publish the same values.  The
+  // attention routines call read_pending after their first loads are out.
   int32_t* seq_ctr = &a.seq_cnt[(long long)b * kCntStride];
-  if (tid == 0) __hip_atomic_fetch_add(seq_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int seq_full = a.HK * a.nch;
+  int par = 0;
+  auto read_pending = [&]() {
+    Pending<G> pd;
+    par = a.pend_par[b] & 1;
+    const int pend_rows = a.pend_len[b];
+    pd.rows = pend_rows > 0 ? min(pend_rows, n) : 0;
+    pd.gamma = a.pend_gamma[b];
+    pd.scale = a.pend_scale[b];
+    pd.score = a.score + ck.segrow0;
+    pd.stat = a.segstat + (long long)seg * 2 * G;
+    pd.q = reinterpret_cast<const char*>(a.qprev) + par * qhalf + qgroup;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    if (tid == 0) __hip_atomic_fetch_add(seq_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return pd;
+  };
   auto publish = [&](int seen) {
     if (seen != seq_full) return;
     if (app) a.len[b] = n_att;
@@ -764,24 +784,17 @@ __device__ inline void decode_body(const DecodeArgs& a) {
     __hip_atomic_store(seq_ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   };
 
-  if (c == 0) {
-    // Keep this step's queries of the group for the next call's score update.
-    const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.q) + qgroup);
-    uint4* dst = reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.qprev) + (par ^ 1) * qhalf + qgroup);
-    for (int i = tid; i < (int)(G * D * sizeof(T) / 16); i += kThreads) dst[i] = src[i];
-  }
   {
-    Pending<G> pd;
-    pd.rows = pend_rows > 0 ? min(pend_rows, n) : 0;
-    pd.score = a.score + ck.segrow0;
-    pd.stat = a.segstat + (long long)seg * 2 * G;
-    pd.q = reinterpret_cast<const char*>(a.qprev) + par * qhalf + qgroup;
-    pd.gamma = pend_gamma;
-    pd.scale = pend_scale;
     if constexpr (sizeof(T) == 2)
-      attn_chunk_mfma<D, G>(a, ck, pd, S.vtiles, S.cb);
+      attn_chunk_mfma<D, G>(a, ck, read_pending, S.vtiles, S.cb);
     else
-      attn_chunk_f32<D, G>(a, ck, pd, S.cb);
+      attn_chunk_f32<D, G>(a, ck, read_pending, S.cb);
+    if (c == 0) {
+      // Keep this step's queries of the group for the next call's score update.
+      const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.q) + qgroup);
+      uint4* dst = reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.qprev) + (par ^ 1) * qhalf + qgroup);
+      for (int i = tid; i < (int)(G * D * sizeof(T) / 16); i += kThreads) dst[i] = src[i];
+    }
     if (a.nch == 1) {
       int seen = 0;
       if (tid == 0) seen = __hip_atomic_load(seq_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
