@@ -13,6 +13,11 @@ then one prune round over all layers.  The default run (1 warm-up step + 15
 timed steps) covers the 8192 generated tokens of the workload; inputs are
 resident in HBM before the timed region starts.
 
+--config 3 runs the Qwen-7B-shaped workload instead (28 layers, 28 query / 4
+KV heads, batch 16, 16k cached tokens, 2048 generated, 30% budget, prune every
+256, recent 256).  Every line also reports what each prune round costs against
+the decode time it saves over the next interval (prune_vs_saved).
+
 Prune rounds (--policy):
   lethe         lethe_layer_sparsity, lethe_rasr_select (a kept set per KV
                 head), lethe_kv_compact -- the default, the headline line;
@@ -61,7 +66,10 @@ KERNEL_SOURCES = ("paper_2511_06029_amd/csrc/decode_attn.hip", "paper_2511_06029
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=15, help="timed prune intervals")
+    ap.add_argument("--config", type=int, choices=(2, 3), default=2,
+                    help="2: Llama-3-8B shapes batch 8 (default); 3: Qwen-7B shapes batch 16, 16k cached")
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed prune intervals (default: the workload's generated tokens minus warm-up)")
     ap.add_argument("--warmup", type=int, default=1, help="untimed prune intervals")
     ap.add_argument("--interval", type=int, default=None, help="decode steps per prune interval (512)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
@@ -94,11 +102,13 @@ def main():
     from workloads import CONFIGS
     from workloads.synth import ZipfCache
 
-    cfg = CONFIGS[2]
+    cfg = CONFIGS[args.config]
     dev = "cuda"
     torch.cuda.set_device(0)
     Lyr, B, HQ, HK, D = cfg.num_layers, cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
     interval = args.interval or cfg.prune_every
+    if args.steps is None:
+        args.steps = max(1, cfg.decode_steps // interval - args.warmup)
     windows = args.warmup + args.steps
     T0 = cfg.prompt
     cap = T0 + interval * windows
@@ -111,7 +121,7 @@ def main():
 
     log("allocating cache: %d layers x %d seqs x %d kv heads x %d rows" % (Lyr, B, HK, cap))
     cache = L.LetheCache(Lyr, [cap] * B, HQ, HK, D, dtype="bf16", device=dev)
-    gen = ZipfCache(2, device=dev)
+    gen = ZipfCache(args.config, device=dev)
     for l in range(Lyr):
         for b in range(B):
             K, V = gen.segment(l, b, T0, T=T0)
@@ -223,7 +233,7 @@ def main():
     avg_call_s = float(np.sum(decode_ms)) / 1e3 / n_calls
     avg_call_bytes = (tokens * row_bytes + n_calls * fixed_bytes) / n_calls
     achieved = avg_call_bytes / avg_call_s / 1e9
-    traffic = load_traffic(avg_call_bytes)
+    traffic = load_traffic(avg_call_bytes) if args.config == 2 and args.policy == "lethe" else None
 
     # Selection reads every live score once per KV head and writes a mask
     # byte per row and head (lengths at the end of each interval, before
@@ -234,14 +244,41 @@ def main():
     select_gbs = sel_rows * HK * 5 / (float(np.sum(select_ms)) / 1e3) / 1e9
 
     value = tokens / elapsed
-    workload = "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128"
+    # What each prune round costs against the decode time it saves over the
+    # next interval: per-step decode time is fit as a + b * (cached tokens)
+    # over every interval of the run (warm-up included), and round w saves
+    # interval * b * (tokens it evicted).
+    all_dec = np.array([win_ev[w][0].elapsed_time(win_ev[w][1]) for w in range(windows)]) / interval
+    all_prune = np.array([win_ev[w][1].elapsed_time(win_ev[w][4]) for w in range(windows)])
+    start_rows = np.array([int(len_snap[w].numpy().astype(np.int64).sum()) for w in range(windows + 1)])
+    mid_rows = start_rows[:windows] + Lyr * B * (interval + 1) / 2.0
+    prune_vs_saved = None
+    if windows >= 2 and np.ptp(mid_rows) > 0:
+        slope, icpt = np.polyfit(mid_rows, all_dec, 1)
+        ratios = []
+        for w in range(windows):
+            evicted = start_rows[w] + Lyr * B * interval - start_rows[w + 1]
+            saved_ms = interval * slope * evicted
+            ratios.append(float(all_prune[w] / saved_ms) if saved_ms > 0 else None)
+        steady = [r for r in ratios[1:] if r is not None]
+        prune_vs_saved = {
+            "round1": ratios[0], "steady_median": float(np.median(steady)) if steady else None,
+            "per_round": ratios, "decode_ms_per_token_step": float(slope), "decode_step_fixed_ms": float(icpt),
+            "prune_round_ms": [float(x) for x in all_prune],
+        }
+    if args.config == 2:
+        workload = "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128"
+    else:
+        workload = "qwen7b-shapes batch 16, 16k cached + generated tokens, 30% budget, prune every 256, recent 256"
     if args.policy == "lethe-shared":
         workload += ", one kept set per layer and sequence"
     elif args.policy in ("h2o", "streaming", "pyramid"):
         workload = workload.replace("40% budget", "40%% budget, %s rule" % args.policy)
     elif args.policy == "shrink":
-        workload = ("llama3-8b-shapes batch 8, 2k prompt + generated tokens, Algorithm 1 shrinking every 512 "
-                    "(D=%d, tau=%g, recent 128, first threshold 2048)" % (args.segments, args.tau))
+        workload = ("%s-shapes batch %d, %d cached + generated tokens, Algorithm 1 shrinking every %d "
+                    "(D=%d, tau=%g, recent %d, first threshold %d)" % (
+                        "llama3-8b" if args.config == 2 else "qwen7b", B, T0, interval, args.segments, args.tau,
+                        recent, T0))
     result = {
         "metric": "KV tokens scanned/s (fused decode-attn+score, prune rounds included)",
         "value": value,
@@ -270,11 +307,12 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS, "traffic": traffic and traffic["bytes"],
-            "kernel": "decode_bf16_kernel<128, 4> (lethe_decode_attn_score, one launch per layer call)",
+            "kernel": "decode_bf16_kernel<%d, %d> (lethe_decode_attn_score, one launch per layer call)" % (D, HQ // HK),
             "bytes_per_launch": avg_call_bytes, "launches": n_calls,
             "traffic_source": traffic and traffic["source"],
         },
         "final_lengths_mean": float(len_snap[windows].numpy().mean()),
+        "prune_vs_saved": prune_vs_saved,
     }
 
     if not args.no_cpu_baseline:

@@ -5,7 +5,8 @@
 // vectors of the live rows once (4 bytes per row), forms a_j = sum_h s_h,j in
 // fp64, and reduces |a|_1 and |a|_2^2 in fp64 (the score vectors of a layer can
 // hold 10^5 rows of widely varying magnitude).
-// budget_kernel: one thread per sequence runs the split over <= 256 layers.
+// budget_kernel: one wavefront per sequence runs the split, a lane per layer
+// (up to four layers a lane for L <= 256).
 #include <math.h>
 
 #include "device_common.h"
@@ -65,87 +66,137 @@ __global__ __launch_bounds__(kThreads) void hoyer_kernel(SparsityArgs a) {
   }
 }
 
-// Proportional integer split with floors and caps (see lethe.h).
-__global__ void budget_kernel(SparsityArgs a) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= a.B) return;
+// Proportional integer split with floors and caps (see lethe.h).  One
+// wavefront per sequence; lane x holds layers x, x + 64, ... (at most
+// kMaxLayers / 64 per lane, unrolled into registers).  All quotas of a pass
+// are taken against the same R and W, as the rule says; the leftover tokens
+// go to the layers whose rank by (remainder desc, layer asc) is below the
+// leftover count.
+constexpr int kLpl = kMaxLayers / kWave;  // layers per lane
+
+__device__ inline unsigned long long wave_sum_u64(unsigned long long v) {
+  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__global__ __launch_bounds__(kWave) void budget_kernel(SparsityArgs a) {
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
   const int L = a.L;
-  long long f[kMaxLayers], cp[kMaxLayers];
-  unsigned long long w[kMaxLayers], rem[kMaxLayers];
-  unsigned char act[kMaxLayers], pick[kMaxLayers];
+  long long f[kLpl], cp[kLpl];
+  unsigned long long w[kLpl], rem[kLpl];
+  int out[kLpl];
+  bool act[kLpl];
   long long sum_n = 0, sum_f = 0;
-  int* out = a.budget_out + (long long)b * L;
   const float* Sp = a.sparsity_in ? a.sparsity_in : a.sparsity_out;
-  for (int l = 0; l < L; ++l) {
+#pragma unroll
+  for (int k = 0; k < kLpl; ++k) {
+    const int l = lane + kWave * k;
+    f[k] = cp[k] = 0;
+    w[k] = 0;
+    rem[k] = 0;
+    act[k] = false;
+    out[k] = 0;
+    if (l >= L) continue;
     long long nl = a.len[(long long)l * a.B + b];
     if (nl < 0) nl = 0;
     long long fl = (long long)a.recent + (long long)a.sink;
     if (fl > nl) fl = nl;
-    f[l] = fl;
-    cp[l] = nl;
+    f[k] = fl;
+    cp[k] = nl;
     sum_n += nl;
     sum_f += fl;
     float S = Sp[(long long)b * L + l];
     if (a.sparsity_in) a.sparsity_out[(long long)b * L + l] = S;
     if (!(S >= 0.0f)) S = 0.0f;
     if (S > 1.0f) S = 1.0f;
-    float scaled = __fmul_rn(__fsub_rn(1.0f, S), 16777216.0f);
-    w[l] = 1ull + (unsigned long long)(unsigned int)floorf(scaled);
+    const float scaled = __fmul_rn(__fsub_rn(1.0f, S), 16777216.0f);
+    w[k] = 1ull + (unsigned long long)(unsigned int)floorf(scaled);
   }
+  sum_n = (long long)wave_sum_u64((unsigned long long)sum_n);
+  sum_f = (long long)wave_sum_u64((unsigned long long)sum_f);
+  int* outp = a.budget_out + (long long)b * L;
   const long long G = a.global_budget[b];
   if (sum_n <= G || sum_f > G) {
-    for (int l = 0; l < L; ++l) out[l] = (int)cp[l];
-    if (sum_n > G) atomicOr(a.dev_status, LETHE_DEV_INFEASIBLE);
+#pragma unroll
+    for (int k = 0; k < kLpl; ++k)
+      if (lane + kWave * k < L) outp[lane + kWave * k] = (int)cp[k];
+    if (sum_n > G && lane == 0) atomicOr(a.dev_status, LETHE_DEV_INFEASIBLE);
     return;
   }
   unsigned long long R = (unsigned long long)(G - sum_f);
-  for (int l = 0; l < L; ++l) {
-    act[l] = cp[l] > f[l];
-    out[l] = (int)f[l];
+#pragma unroll
+  for (int k = 0; k < kLpl; ++k) {
+    act[k] = cp[k] > f[k];
+    out[k] = (int)f[k];
   }
   for (;;) {
-    unsigned long long W = 0;
-    for (int l = 0; l < L; ++l)
-      if (act[l]) W += w[l];
-    bool capped = false;
-    for (int l = 0; l < L; ++l) {
-      pick[l] = 0;
-      if (!act[l]) continue;
-      unsigned long long ql = (R * w[l]) / W;
-      if ((unsigned long long)f[l] + ql >= (unsigned long long)cp[l]) pick[l] = 1, capped = true;
+    unsigned long long wa = 0;
+#pragma unroll
+    for (int k = 0; k < kLpl; ++k) wa += act[k] ? w[k] : 0ull;
+    const unsigned long long W = wave_sum_u64(wa);
+    unsigned long long q[kLpl];
+    bool capped_any = false;
+    unsigned long long taken = 0;
+#pragma unroll
+    for (int k = 0; k < kLpl; ++k) {
+      q[k] = act[k] ? (R * w[k]) / W : 0ull;
+      const bool cap_k = act[k] && (unsigned long long)f[k] + q[k] >= (unsigned long long)cp[k];
+      capped_any |= cap_k;
+      if (cap_k) taken += (unsigned long long)(cp[k] - f[k]);
     }
-    if (capped) {
-      unsigned long long taken = 0;
-      for (int l = 0; l < L; ++l) {
-        if (!pick[l]) continue;
-        out[l] = (int)cp[l];
-        taken += (unsigned long long)(cp[l] - f[l]);
-        act[l] = 0;
+    if (__any(capped_any)) {
+      // Every layer that reaches its cap in this pass is fixed at once.
+#pragma unroll
+      for (int k = 0; k < kLpl; ++k) {
+        if (act[k] && (unsigned long long)f[k] + q[k] >= (unsigned long long)cp[k]) {
+          out[k] = (int)cp[k];
+          act[k] = false;
+        }
       }
-      R -= taken;
+      R -= wave_sum_u64(taken);
       continue;
     }
     unsigned long long given = 0;
-    for (int l = 0; l < L; ++l) {
-      if (!act[l]) continue;
-      unsigned long long ql = (R * w[l]) / W;
-      rem[l] = (R * w[l]) % W;
-      out[l] = (int)(f[l] + (long long)ql);
-      given += ql;
-      pick[l] = 0;
+#pragma unroll
+    for (int k = 0; k < kLpl; ++k) {
+      if (!act[k]) continue;
+      rem[k] = (R * w[k]) % W;
+      out[k] = (int)(f[k] + (long long)q[k]);
+      given += q[k];
     }
-    unsigned long long left = R - given;
-    for (unsigned long long t = 0; t < left; ++t) {
-      int best = -1;
-      for (int l = 0; l < L; ++l) {
-        if (!act[l] || pick[l]) continue;
-        if (best < 0 || rem[l] > rem[best]) best = l;
+    const unsigned long long left = R - wave_sum_u64(given);
+    // Rank of each active layer among the active layers by (remainder desc,
+    // layer asc); the first `left` of them get one more token.
+    int rank[kLpl];
+#pragma unroll
+    for (int k = 0; k < kLpl; ++k) rank[k] = 0;
+    for (int j = 0; j < L; ++j) {
+      const int jl = j % kWave, jk = j / kWave;
+      unsigned long long rj = 0;
+      bool aj = false;
+#pragma unroll
+      for (int k = 0; k < kLpl; ++k) {
+        if (k == jk) {
+          rj = __shfl(rem[k], jl);
+          aj = __shfl(act[k] ? 1 : 0, jl) != 0;
+        }
       }
-      pick[best] = 1;
-      out[best] += 1;
+      if (!aj) continue;
+#pragma unroll
+      for (int k = 0; k < kLpl; ++k) {
+        const int l = lane + kWave * k;
+        if (act[k] && (rj > rem[k] || (rj == rem[k] && j < l))) ++rank[k];
+      }
     }
+#pragma unroll
+    for (int k = 0; k < kLpl; ++k)
+      if (act[k] && (unsigned long long)rank[k] < left) out[k] += 1;
     break;
   }
+#pragma unroll
+  for (int k = 0; k < kLpl; ++k)
+    if (lane + kWave * k < L) outp[lane + kWave * k] = out[k];
 }
 
 }  // namespace
@@ -155,8 +206,7 @@ lethe_status launch_sparsity(const SparsityArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(hoyer_kernel, dim3(a.B * a.L), dim3(kThreads), 0, s, a);
     if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
   }
-  const int t = 64;
-  hipLaunchKernelGGL(budget_kernel, dim3((a.B + t - 1) / t), dim3(t), 0, s, a);
+  hipLaunchKernelGGL(budget_kernel, dim3(a.B), dim3(kWave), 0, s, a);
   if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
   return LETHE_OK;
 }
