@@ -903,6 +903,95 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
   }
 }
 
+// bf16 flush on the matrix cores, the pending-update half of the decode
+// loop on its own: one block per (layer, sequence, KV head); wave w takes the
+// 32-row steps w, w + 4, ...; each step's K rows load straight into the
+// operand registers (the next step's while this one computes), S = Q_prev K^T
+// by MFMA, and s <- gamma s + sum_g exp2(scale x_g - M_g) / L_g.
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
+  using Cfg = MfmaCfg<D>;
+  constexpr int KK = Cfg::KK, ROWB = Cfg::ROWB, STEP = Cfg::STEP;
+  static_assert(G <= 8, "pending heads live in lane groups 0 and 1");
+  const int lb = blockIdx.x / a.HK;
+  const int h = blockIdx.x - lb * a.HK;
+  const int l = lb / a.B;
+  const int b = lb - l * a.B;
+  const int P = a.pend_len[lb];
+  if (P <= 0) return;
+  const int n = a.len[lb];
+  const int cp = a.cap[b];
+  const long long sbase = a.seq_base[b];
+  if (n < 0 || cp < 0 || n > cp || sbase < 0 || sbase + (long long)a.HK * cp > a.rows_per_layer) return;
+  const int rows = min(P, n);
+  if (rows <= 0) return;
+  const int par = a.pend_par[lb] & 1;
+  const float gamma = a.pend_gamma[lb];
+  const float scale = a.pend_scale[lb];
+  const int HQ = a.HK * G;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = threadIdx.x / kWave;
+  const int g4 = lane >> 4;
+  const int s = lane & 15;
+  const long long segrow0 = (long long)l * a.rows_per_layer + sbase + (long long)h * cp;
+  const char* qg = reinterpret_cast<const char*>(a.qprev) +
+                   ((((long long)l * 2 + par) * a.B + b) * HQ + (long long)h * G) * D * 2;
+  const float* st = a.segstat + ((long long)lb * a.HK + h) * 2 * G;
+  bf16x8_t qo[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) qo[kk] = q_operand<D, G>(qg, s, g4, kk);
+  float pm[4], pi[4];
+#pragma unroll
+  for (int rr = 0; rr < 4; ++rr) {
+    const int hh = 4 * g4 + rr;
+    pm[rr] = hh < G ? st[hh] : 0.0f;
+    pi[rr] = hh < G ? st[G + hh] : 0.0f;
+  }
+  const char* Kb = reinterpret_cast<const char*>(a.k) + segrow0 * ROWB;
+  float* sc = a.score + segrow0;
+  const int nsteps = (rows + STEP - 1) / STEP;
+
+  bf16x8_t kn[2][KK];
+  float sn = 0.0f;
+  auto load = [&](int bs) {
+#pragma unroll
+    for (int T = 0; T < 2; ++T) {
+      const int row = min(bs + 16 * T + s, rows - 1);
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        kn[T][kk] = *reinterpret_cast<const bf16x8_t*>(Kb + (long long)row * ROWB + 64 * kk + 16 * g4);
+    }
+    sn = g4 < 2 ? sc[min(bs + 16 * g4 + s, rows - 1)] : 0.0f;
+  };
+  int idx = w;
+  if (idx < nsteps) load(idx * STEP);
+  while (idx < nsteps) {
+    bf16x8_t kc[2][KK];
+#pragma unroll
+    for (int T = 0; T < 2; ++T)
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) kc[T][kk] = kn[T][kk];
+    const float sold = sn;
+    const int base = idx * STEP;
+    const int nidx = idx + kNumWaves;
+    if (nidx < nsteps) load(nidx * STEP);
+    float part[2];
+#pragma unroll
+    for (int T = 0; T < 2; ++T) {
+      f32x4_t so = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) so = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qo[kk], kc[T][kk], so, 0, 0, 0);
+      float acc = 0.0f;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) acc = fmaf(hw_exp2(fmaf(so[rr], scale, -pm[rr])), pi[rr], acc);
+      part[T] = acc + __shfl_xor(acc, 16);
+    }
+    const int prow = base + 16 * g4 + s;
+    if (g4 < 2 && prow < rows) sc[prow] = fmaf(gamma, sold, g4 == 0 ? part[0] : part[1]);
+    idx = nidx;
+  }
+}
+
 __global__ void flush_clear_kernel(int32_t* pend_len, int count) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) pend_len[i] = 0;
@@ -971,7 +1060,10 @@ lethe_status launch_td(const DecodeArgs& a, int G, hipStream_t s) {
 
 template <typename T, int D, int G>
 lethe_status launch_flush_tdg(const FlushArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((flush_kernel<T, D, G>), dim3((unsigned)(a.L * a.B * a.HK)), dim3(kThreads), 0, s, a);
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL((flush_bf16_kernel<D, G>), dim3((unsigned)(a.L * a.B * a.HK)), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((flush_kernel<T, D, G>), dim3((unsigned)(a.L * a.B * a.HK)), dim3(kThreads), 0, s, a);
   if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
   const int count = a.L * a.B;
   hipLaunchKernelGGL(flush_clear_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, a.pend_len, count);
