@@ -2,14 +2,15 @@
 //
 // One block per (layer, sequence, KV head) segment.  Rows before the first
 // evicted row stay where they are.  From there the block sweeps the source rows
-// in tiles of 64: one wavefront ballots the keep flags of the tile and writes
-// the kept rows' source indices, in order, to LDS; every thread copies its
-// share of those rows (16 bytes per lane) into an LDS stage, the block
-// synchronises, and the staged rows are stored to their destinations (a
-// running prefix count).  A destination never exceeds its source, and the
-// stores of a tile only reach rows below the tile's end, so no tile overwrites
-// a row that a later tile still has to read; within a tile, every load has
-// delivered its data to LDS before the barrier that precedes the stores.
+// in tiles of 128: two wavefronts ballot the keep flags of the tile and list
+// the kept rows' source indices in LDS; every thread loads its share of those
+// rows (16 bytes per lane) into registers, waits for its loads, the block
+// synchronises, and the rows are stored to their destinations (a running
+// prefix count).  A destination never exceeds its source, and the stores of a
+// tile only reach rows below the tile's end, so no tile overwrites a row that
+// a later tile still has to read; within a tile, every load has completed
+// before the barrier that precedes the stores.  The next tile's keep flags
+// are read before the current tile's stores go out.
 #include "device_common.h"
 #include "lethe_internal.h"
 
@@ -18,7 +19,10 @@ namespace lethe {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTile = 64;
+constexpr int kTile = 128;
+constexpr int kTileWaves = kTile / kWave;
+// 16 bytes of a row; a vector type, so arrays of them stay in registers.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
 template <int RB>  // row bytes of K (= of V)
 __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
@@ -49,11 +53,8 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
 
   // First evicted row.
   __shared__ int s_first;
-  __shared__ int s_dst[kTile];
-  __shared__ int s_cnt;
-  __shared__ uint4 stage_k[kTile][TPR];
-  __shared__ uint4 stage_v[kTile][TPR];
-  __shared__ float stage_s[kTile];
+  __shared__ int s_src[kTile];          // per ballot wave: its kept rows in order
+  __shared__ int s_cnt[kTileWaves];
   if (tid == 0) s_first = n;
   __syncthreads();
   {
@@ -69,46 +70,60 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   const int first = s_first;
   int pos = first;  // next destination row
   const int lane = tid & (kWave - 1);
+  const int w = tid / kWave;
+  const int sub = tid % TPR;
+  bool kp_next = tid < kTile && first + tid < n && keep[first + tid] != 0;
   for (int j0 = first; j0 < n; j0 += kTile) {
-    if (tid < kWave) {
-      const int j = j0 + lane;
-      const bool kp = j < n && keep[j] != 0;
+    if (tid < kTile) {
+      const bool kp = kp_next;
       const unsigned long long mask = __ballot(kp);
       const int before = __popcll(mask & ((1ull << lane) - 1ull));
-      const int cnt = __popcll(mask);
-      // s_dst[i] = source row of the i-th kept row of the tile.
-      if (kp) s_dst[before] = j;
-      if (lane == 0) s_cnt = cnt;
+      if (kp) s_src[kWave * w + before] = j0 + tid;
+      if (lane == 0) s_cnt[w] = __popcll(mask);
     }
     __syncthreads();
-    const int cnt = s_cnt;
-    const int sub = tid % TPR;
-    // Stage the kept rows of the tile in LDS.  Each load's data has arrived
-    // before it is written to LDS, and the barrier after the LDS writes
-    // precedes every global store of the tile.
+    int cw[kTileWaves];
+    int cnt = 0;
+#pragma unroll
+    for (int x = 0; x < kTileWaves; ++x) {
+      cw[x] = s_cnt[x];
+      cnt += cw[x];
+    }
+    u32x4_t rk[PASSES], rv[PASSES];
+    float rs[PASSES];
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
       const int i = p * RPP + tid / TPR;
       if (i < cnt) {
-        const long long src = s_dst[i];
-        stage_k[i][sub] = *reinterpret_cast<const uint4*>(K + src * RB + sub * 16);
-        stage_v[i][sub] = *reinterpret_cast<const uint4*>(V + src * RB + sub * 16);
+        int x = 0, off = i;
+#pragma unroll
+        for (int y = 0; y + 1 < kTileWaves; ++y)
+          if (x == y && off >= cw[y]) {
+            off -= cw[y];
+            x = y + 1;
+          }
+        const long long src = s_src[kWave * x + off];
+        rk[p] = *reinterpret_cast<const u32x4_t*>(K + src * RB + sub * 16);
+        rv[p] = *reinterpret_cast<const u32x4_t*>(V + src * RB + sub * 16);
+        rs[p] = sub == 0 ? S[src] : 0.0f;
       }
     }
-    if (tid < cnt) stage_s[tid] = S[s_dst[tid]];
-    __syncthreads();
+    // The next tile's keep flags (a separate array: no ordering with the rows).
+    const int jn = j0 + kTile + tid;
+    kp_next = tid < kTile && jn < n && keep[jn] != 0;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // every load of the tile has completed; s_src may be reused
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
       const int i = p * RPP + tid / TPR;
       if (i < cnt) {
         const long long dst = pos + i;
-        *reinterpret_cast<uint4*>(K + dst * RB + sub * 16) = stage_k[i][sub];
-        *reinterpret_cast<uint4*>(V + dst * RB + sub * 16) = stage_v[i][sub];
+        *reinterpret_cast<u32x4_t*>(K + dst * RB + sub * 16) = rk[p];
+        *reinterpret_cast<u32x4_t*>(V + dst * RB + sub * 16) = rv[p];
+        if (sub == 0) S[dst] = rs[p];
       }
     }
-    if (tid < cnt) S[pos + tid] = stage_s[tid];
     pos += cnt;
-    __syncthreads();  // s_dst, s_cnt and the stage are rewritten by the next tile
   }
   if (tid == 0) a.counts[cidx] = pos;
 }
