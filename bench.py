@@ -15,7 +15,10 @@ resident in HBM before the timed region starts.
 
 --config 3 runs the Qwen-7B-shaped workload instead (28 layers, 28 query / 4
 KV heads, batch 16, 16k cached tokens, 2048 generated, 30% budget, prune every
-256, recent 256).  Every line also reports what each prune round costs against
+256, recent 256); --config 4 and 5 the ragged Llama-3-8B batches (64
+sequences of U[8k, 32k] cached tokens; 128 sequences of logU[1k, 64k] with
+fixed layer shares, started from the steady state since their full caches
+do not fit one GPU with headroom).  Every line also reports what each prune round costs against
 the decode time it saves over the next interval (prune_vs_saved).
 
 Prune rounds (--policy):
@@ -66,8 +69,10 @@ KERNEL_SOURCES = ("paper_2511_06029_amd/csrc/decode_attn.hip", "paper_2511_06029
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--config", type=int, choices=(2, 3), default=2,
-                    help="2: Llama-3-8B shapes batch 8 (default); 3: Qwen-7B shapes batch 16, 16k cached")
+    ap.add_argument("--config", type=int, choices=(2, 3, 4, 5), default=2,
+                    help="2: Llama-3-8B shapes batch 8 (default); 3: Qwen-7B shapes batch 16, 16k cached; "
+                         "4: Llama-3-8B batch 64, lengths U[8k, 32k]; 5: Llama-3-8B batch 128, lengths "
+                         "logU[1k, 64k], fixed layer shares, from the steady state")
     ap.add_argument("--steps", type=int, default=None,
                     help="timed prune intervals (default: the workload's generated tokens minus warm-up)")
     ap.add_argument("--warmup", type=int, default=1, help="untimed prune intervals")
@@ -110,8 +115,6 @@ def main():
     if args.steps is None:
         args.steps = max(1, cfg.decode_steps // interval - args.warmup)
     windows = args.warmup + args.steps
-    T0 = cfg.prompt
-    cap = T0 + interval * windows
     recent, sink = cfg.recent, cfg.sink
     policy = None if args.policy == "shrink" else policies.get(args.policy, gamma=cfg.gamma, sink=sink)
     gamma = policy.gamma if policy else cfg.gamma
@@ -119,32 +122,63 @@ def main():
     def log(msg):
         print("[bench] " + msg, file=sys.stderr, flush=True)
 
-    log("allocating cache: %d layers x %d seqs x %d kv heads x %d rows" % (Lyr, B, HK, cap))
-    cache = L.LetheCache(Lyr, [cap] * B, HQ, HK, D, dtype="bf16", device=dev)
     gen = ZipfCache(args.config, device=dev)
+    T = gen.lengths().astype(np.int64)          # logical length of every sequence at the start
+    T0 = int(T.max())
+    static_s = None
+    if cfg.zipf == "fixed_weights":
+        # Fixed layer shares (2%..40%, mean 10%) through sparsity_in; the full
+        # cache of this workload does not fit one GPU with headroom, so the run
+        # starts from the steady state: every layer holds its budget share.
+        shares, static_s = gen.layer_weights()
+        floor_rows = recent + sink
+        n_init = np.zeros((Lyr, B), np.int64)
+        for b in range(B):
+            G_b = int(math.floor(cfg.budget_frac * T[b])) * Lyr
+            n_init[:, b] = np.clip(np.floor(floor_rows + (G_b - floor_rows * Lyr) * shares / shares.sum()),
+                                   min(T[b], floor_rows), T[b])
+    else:
+        n_init = np.tile(T, (Lyr, 1))
+    caps = [int(n_init[:, b].max()) + interval * windows + 1 for b in range(B)]
+    log("allocating cache: %d layers x %d seqs x %d kv heads, %d rows per layer" % (Lyr, B, HK, HK * sum(caps)))
+    cache = L.LetheCache(Lyr, caps, HQ, HK, D, dtype="bf16", device=dev)
     for l in range(Lyr):
         for b in range(B):
-            K, V = gen.segment(l, b, T0, T=T0)
+            n = int(n_init[l, b])
+            K, V = gen.segment(l, b, n, T=int(T[b]))
             for h in range(HK):
                 s0, _ = cache.seg_rows(b, h)
-                cache.k[l, s0:s0 + T0] = K[h]
-                cache.v[l, s0:s0 + T0] = V[h]
-    cache.len.fill_(T0)
+                cache.k[l, s0:s0 + n] = K[h]
+                cache.v[l, s0:s0 + n] = V[h]
+            del K, V
+    cache.len.copy_(torch.from_numpy(n_init.astype(np.int32)).to(dev))
+    # Decode-step inputs: 32 sets per epoch of the query direction (one epoch
+    # unless the heavy hitters drift), reused cyclically within an epoch.
     P = 32
-    log("generating %d decode-step input sets" % P)
-    qp = torch.empty((P, Lyr, B, HQ, D), dtype=torch.bfloat16, device=dev)
-    kp = torch.empty((P, Lyr, B, HK, D), dtype=torch.bfloat16, device=dev)
-    vp = torch.empty((P, Lyr, B, HK, D), dtype=torch.bfloat16, device=dev)
-    for t in range(P):
-        for l in range(Lyr):
-            q, k, v = gen.step(t, l, T=np.full(B, T0))
-            qp[t, l], kp[t, l], vp[t, l] = q, k, v
+    epoch = cfg.epoch if (cfg.zipf == "drift" and cfg.epoch > 0) else 0
+    E = max(1, -(-(interval * windows) // epoch)) if epoch else 1
+    log("generating %d x %d decode-step input sets" % (E, P))
+    qp = torch.empty((E * P, Lyr, B, HQ, D), dtype=torch.bfloat16, device=dev)
+    kp = torch.empty((E * P, Lyr, B, HK, D), dtype=torch.bfloat16, device=dev)
+    vp = torch.empty((E * P, Lyr, B, HK, D), dtype=torch.bfloat16, device=dev)
+    for e in range(E):
+        for t in range(P):
+            for l in range(Lyr):
+                q, k, v = gen.step(e * epoch + t, l, T=T)
+                qp[e * P + t, l], kp[e * P + t, l], vp[e * P + t, l] = q, k, v
     out = torch.empty((B, HQ, D), dtype=torch.float32, device=dev)
     ws = cache.workspace(L.OP_DECODE)
     ws_c = cache.workspace(L.OP_COMPACT)
     keep = torch.empty((Lyr, cache.rows_per_layer), dtype=torch.uint8, device=dev)
     prune = policies.PruneRound(cache, policy) if policy else None
-    evict = torch.full((Lyr, B), T0, dtype=torch.int32, device=dev)
+    if prune is not None and static_s is not None and policy.layer_budget == "sparsity":
+        prune.s_in = torch.from_numpy(np.tile(static_s, (B, 1))).to(dev)
+    evict = torch.from_numpy(n_init.astype(np.int32)).to(dev)
+    # Per-layer budget of every sequence at every round, on the device ahead
+    # of the timed loop: floor(rho * T_b) at the round's logical length.
+    per_layer_all = np.array([[policies.per_layer_budget(cfg.budget_frac, int(T[b] + (w + 1) * interval))
+                               for b in range(B)] for w in range(windows)], np.int64)
+    per_layer_dev = torch.from_numpy(per_layer_all).to(dev)
     torch.cuda.synchronize()
     if args.copy_probe > 0:
         # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings
@@ -164,25 +198,24 @@ def main():
     sp = ctypes.c_void_p(stream.cuda_stream)
     fn = lib.lethe_decode_attn_score
     out_p, ws_p, wsb = ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel()
-    q_ptr = [[ctypes.c_void_p(qp[t, l].data_ptr()) for l in range(Lyr)] for t in range(P)]
-    k_ptr = [[ctypes.c_void_p(kp[t, l].data_ptr()) for l in range(Lyr)] for t in range(P)]
-    v_ptr = [[ctypes.c_void_p(vp[t, l].data_ptr()) for l in range(Lyr)] for t in range(P)]
+    q_ptr = [[ctypes.c_void_p(qp[t, l].data_ptr()) for l in range(Lyr)] for t in range(E * P)]
+    k_ptr = [[ctypes.c_void_p(kp[t, l].data_ptr()) for l in range(Lyr)] for t in range(E * P)]
+    v_ptr = [[ctypes.c_void_p(vp[t, l].data_ptr()) for l in range(Lyr)] for t in range(E * P)]
 
     len_snap = [torch.empty((Lyr, B), dtype=torch.int32, pin_memory=True) for _ in range(windows + 1)]
     win_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(windows)]
 
     def run_window(w, timed):
-        T_start = T0 + w * interval
         len_snap[w].copy_(cache.len, non_blocking=True)
         win_ev[w][0].record(stream)
         for i in range(interval):
-            t = (w * interval + i) % P
+            tg = w * interval + i
+            t = (min(tg // epoch, E - 1) * P if epoch else 0) + tg % P
             for l in range(Lyr):
                 rc = fn(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, ws_p, wsb, sp)
                 if rc != 0:
                     raise RuntimeError("lethe_decode_attn_score: %s" % L.status_string(rc))
         win_ev[w][1].record(stream)
-        T_end = T_start + interval
         if args.policy == "shrink":
             L.score_flush(cache)
             win_ev[w][2].record(stream)
@@ -190,7 +223,10 @@ def main():
             win_ev[w][3].record(stream)
             L.kv_compact(cache, keep, ws_c)
         else:
-            r, sk = prune.budgets(policies.per_layer_budget(cfg.budget_frac, T_end), recent)
+            if policy.window_fills:
+                r, sk = prune.budgets(int(per_layer_all[w].min()), recent)
+            else:
+                r, sk = prune.budgets(per_layer_dev[w], recent)
             win_ev[w][2].record(stream)
             prune.select(r, sk)
             win_ev[w][3].record(stream)
@@ -253,7 +289,9 @@ def main():
     start_rows = np.array([int(len_snap[w].numpy().astype(np.int64).sum()) for w in range(windows + 1)])
     mid_rows = start_rows[:windows] + Lyr * B * (interval + 1) / 2.0
     prune_vs_saved = None
-    if windows >= 2 and np.ptp(mid_rows) > 0:
+    # The fit needs intervals of clearly different sizes (a run that starts
+    # at the steady state has none).
+    if windows >= 2 and np.ptp(mid_rows) >= 0.1 * mid_rows.mean():
         slope, icpt = np.polyfit(mid_rows, all_dec, 1)
         ratios = []
         for w in range(windows):
@@ -266,10 +304,14 @@ def main():
             "per_round": ratios, "decode_ms_per_token_step": float(slope), "decode_step_fixed_ms": float(icpt),
             "prune_round_ms": [float(x) for x in all_prune],
         }
-    if args.config == 2:
-        workload = "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128"
-    else:
-        workload = "qwen7b-shapes batch 16, 16k cached + generated tokens, 30% budget, prune every 256, recent 256"
+    workload = {
+        2: "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128",
+        3: "qwen7b-shapes batch 16, 16k cached + generated tokens, 30% budget, prune every 256, recent 256",
+        4: "llama3-8b-shapes batch 64, cached lengths U[8k, 32k] + generated tokens, drifting heavy hitters, "
+           "25% budget, prune every 256, recent 128",
+        5: "llama3-8b-shapes batch 128, lengths logU[1k, 64k], fixed layer shares 2%-40% (10% budget), "
+           "steady-state start, prune every 128, recent 64",
+    }[args.config]
     if args.policy == "lethe-shared":
         workload += ", one kept set per layer and sequence"
     elif args.policy in ("h2o", "streaming", "pyramid"):
@@ -277,7 +319,7 @@ def main():
     elif args.policy == "shrink":
         workload = ("%s-shapes batch %d, %d cached + generated tokens, Algorithm 1 shrinking every %d "
                     "(D=%d, tau=%g, recent %d, first threshold %d)" % (
-                        "llama3-8b" if args.config == 2 else "qwen7b", B, T0, interval, args.segments, args.tau,
+                        "qwen7b" if args.config == 3 else "llama3-8b", B, T0, interval, args.segments, args.tau,
                         recent, T0))
     result = {
         "metric": "KV tokens scanned/s (fused decode-attn+score, prune rounds included)",
@@ -295,7 +337,8 @@ def main():
         "config": {
             "workload": workload,
             "layers": Lyr, "q_heads": HQ, "kv_heads": HK, "head_dim": D, "batch": B, "storage": "bf16",
-            "prompt": T0, "generated": interval * windows, "interval": interval, "gamma": gamma,
+            "prompt": T0 if cfg.length_dist == "fixed" else "%s%s" % (cfg.length_dist, list(cfg.length_range)),
+            "generated": interval * windows, "interval": interval, "gamma": gamma,
         },
         "decode_step_ms": float(np.mean(decode_ms)) / interval,
         "prune_round_us": float(np.mean(prune_ms)) * 1e3,

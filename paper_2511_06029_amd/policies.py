@@ -107,8 +107,20 @@ class PruneRound:
     def budgets(self, per_layer_budget, recent):
         """Layer sparsity (or the static table) and budgets for a round in
         which sequence b may keep per_layer_budget rows per layer (an int for
-        every sequence, or one int per sequence).  Returns (recent, sink)."""
+        every sequence, one int per sequence, or an int64 device tensor [B]).
+        Returns (recent, sink)."""
         import torch
+        if isinstance(per_layer_budget, torch.Tensor) and per_layer_budget.is_cuda:
+            # Per-sequence budgets already on the device (int64 [B]): no host
+            # round trip inside a timed loop.
+            if self.policy.window_fills:
+                raise ValueError("a window-filling policy needs one host-side budget for every sequence")
+            if per_layer_budget.shape != (self.cache.B,):
+                raise ValueError("one budget per sequence expected")
+            torch.mul(per_layer_budget, self.cache.L, out=self.gbud)
+            r, sk = self.policy.windows(0, recent)
+            L.layer_sparsity(self.cache, self.gbud, r, sk, self.s_in, self.S, self.budget)
+            return r, sk
         if isinstance(per_layer_budget, int):
             per_seq = [per_layer_budget] * self.cache.B
         else:
