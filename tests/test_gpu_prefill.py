@@ -204,3 +204,61 @@ def test_prefill_llama8b_prompt_full_size():
     assert np.isfinite(f32(cs.out)).all()
     cs.check(seqs=[0], heads=[0])
     cs.check(seqs=[B - 1], heads=[HK - 1])
+
+
+def test_prefill_then_decode_and_prune():
+    """Prompt prefill seeds the scores, decode steps decay and extend them
+    (with their deferred updates), then a prune round: the device against the
+    oracle's composition of the same steps."""
+    note("prefill -> decode -> prune")
+    D, G, HK = 128, 4, 2
+    lengths = [300, 701]
+    cs = Case(D, G, HK, lengths, lengths, seed=9)
+    cs.run()
+    c, lay = cs.c, cs.layer
+    B = len(lengths)
+    orc = oracle.OracleCache(2, B, HK * G, HK, D)
+    qh = f32(cs.q)
+    scale = 1.0 / math.sqrt(D)
+    for b, n in enumerate(lengths):
+        r = int(cs.starts[b])
+        for h in range(HK):
+            _, s = oracle.prefill(qh[r:r + n, h * G:(h + 1) * G], cs.K[b, h], cs.V[b, h], None, scale)
+            orc.set_segment(lay, b, h, cs.K[b, h], cs.V[b, h], s)
+    rng = np.random.default_rng(10)
+    ws = c.workspace(L.OP_DECODE)
+    gamma = 0.9
+    for t in range(3):
+        q = torch.from_numpy(rng.standard_normal((B, HK * G, D)).astype(np.float32)).to(DEV).to(torch.bfloat16)
+        kn = torch.from_numpy(rng.standard_normal((B, HK, D)).astype(np.float32)).to(DEV).to(torch.bfloat16)
+        vn = torch.from_numpy(rng.standard_normal((B, HK, D)).astype(np.float32)).to(DEV).to(torch.bfloat16)
+        out = torch.empty((B, HK * G, D), dtype=torch.float32, device=DEV)
+        L.decode_attn_score(c, lay, q, kn, vn, gamma, 0.0, out, ws)
+        ref = orc.decode_step(lay, f32(q), f32(kn), f32(vn), gamma, scale)
+        torch.cuda.synchronize()
+        close(f32(out), ref, "decode out t%d" % t)
+    c.flush()
+    torch.cuda.synchronize()
+    for b, n in enumerate(lengths):
+        for h in range(HK):
+            r0, _ = c.seg_rows(b, h)
+            close(f32(c.score[lay, r0:r0 + n + 3]), orc.s[lay][b][h], "scores b%d h%d" % (b, h))
+    # Prune to 40% per layer, recent 32: masks bit-exact given the device's scores.
+    gb = torch.tensor([int(0.4 * (n + 3)) * 2 for n in lengths], dtype=torch.int64, device=DEV)
+    S = torch.empty((B, 2), dtype=torch.float32, device=DEV)
+    bud = torch.empty((B, 2), dtype=torch.int32, device=DEV)
+    L.layer_sparsity(c, gb, 32, 0, None, S, bud)
+    keep = torch.zeros((2, c.rows_per_layer), dtype=torch.uint8, device=DEV)
+    L.rasr_select(c, bud, 32, 0, keep)
+    torch.cuda.synchronize()
+    bh = bud.cpu().numpy()
+    kh = keep.cpu().numpy()
+    for b, n in enumerate(lengths):
+        for h in range(HK):
+            r0, _ = c.seg_rows(b, h)
+            want = oracle.rasr_select(f32(c.score[lay, r0:r0 + n + 3]), bh[b, lay], 32, 0)
+            np.testing.assert_array_equal(kh[lay, r0:r0 + n + 3].astype(bool), want)
+    L.kv_compact(c, keep, c.workspace(L.OP_COMPACT))
+    torch.cuda.synchronize()
+    assert [int(c.len[lay, b]) for b in range(B)] == [min(n + 3, int(bh[b, lay])) for b, n in enumerate(lengths)]
+    assert int(c.dev_status[0]) == 0
