@@ -84,6 +84,8 @@ def parse():
     ap.add_argument("--segments", type=int, default=10, help="Algorithm 1 segments D (shrink)")
     ap.add_argument("--tau", type=float, default=400.0, help="Algorithm 1 ratio threshold (shrink)")
     ap.add_argument("--prefill", action="store_true", help="time the prompt prefill with score seeding instead")
+    ap.add_argument("--no-settle", action="store_true",
+                    help="last step of an interval deferred like the others (the prune round then applies it)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="first copy MIB MiB device-to-device 3 times (counter calibration runs)")
     return ap.parse_args()
@@ -167,7 +169,9 @@ def main():
                 q, k, v = gen.step(e * epoch + t, l, T=T)
                 qp[e * P + t, l], kp[e * P + t, l], vp[e * P + t, l] = q, k, v
     out = torch.empty((B, HQ, D), dtype=torch.float32, device=dev)
-    ws = cache.workspace(L.OP_DECODE)
+    # One workspace for both decode calls: the settling call's layout starts
+    # with the deferred call's.
+    ws = cache.workspace(L.OP_DECODE if args.no_settle else L.OP_DECODE_FINAL)
     ws_c = cache.workspace(L.OP_COMPACT)
     keep = torch.empty((Lyr, cache.rows_per_layer), dtype=torch.uint8, device=dev)
     prune = policies.PruneRound(cache, policy) if policy else None
@@ -197,6 +201,9 @@ def main():
     stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
     fn = lib.lethe_decode_attn_score
+    # The step before each prune round settles its own score update, so the
+    # round reads no K row to apply it.
+    fn_last = fn if args.no_settle else lib.lethe_decode_attn_score_final
     out_p, ws_p, wsb = ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel()
     q_ptr = [[ctypes.c_void_p(qp[t, l].data_ptr()) for l in range(Lyr)] for t in range(E * P)]
     k_ptr = [[ctypes.c_void_p(kp[t, l].data_ptr()) for l in range(Lyr)] for t in range(E * P)]
@@ -211,8 +218,9 @@ def main():
         for i in range(interval):
             tg = w * interval + i
             t = (min(tg // epoch, E - 1) * P if epoch else 0) + tg % P
+            f = fn_last if i == interval - 1 else fn
             for l in range(Lyr):
-                rc = fn(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, ws_p, wsb, sp)
+                rc = f(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, ws_p, wsb, sp)
                 if rc != 0:
                     raise RuntimeError("lethe_decode_attn_score: %s" % L.status_string(rc))
         win_ev[w][1].record(stream)
@@ -264,7 +272,9 @@ def main():
     select_ms = [win_ev[w][2].elapsed_time(win_ev[w][3]) for w in range(args.warmup, windows)]
     # Roofline of lethe_decode_attn_score: one kernel launch per call, back to
     # back on the launch stream; the events bracket every decode call of the
-    # timed intervals, so their span / calls is the average launch duration.
+    # timed intervals, so their span / calls is the average launch duration
+    # (the settling calls' second, small kernel included: one step in an
+    # interval).
     n_calls = args.steps * interval * Lyr
     avg_call_s = float(np.sum(decode_ms)) / 1e3 / n_calls
     avg_call_bytes = (tokens * row_bytes + n_calls * fixed_bytes) / n_calls
@@ -343,6 +353,7 @@ def main():
         "decode_step_ms": float(np.mean(decode_ms)) / interval,
         "prune_round_us": float(np.mean(prune_ms)) * 1e3,
         "policy": args.policy,
+        "settled_last_step": not args.no_settle,
         "select_us": float(np.mean(select_ms)) * 1e3,
         "select_hbm_gbs": select_gbs,
         "decode_call_us": avg_call_s * 1e6,

@@ -96,6 +96,7 @@ typedef struct {
 #define LETHE_OP_SPARSITY 1
 #define LETHE_OP_SELECT 2
 #define LETHE_OP_COMPACT 3
+#define LETHE_OP_DECODE_FINAL 4
 
 /*
  * Bytes of device workspace `op` needs for this cache (0 when none).  No
@@ -163,6 +164,26 @@ lethe_status lethe_decode_attn_score(const lethe_cache* cache, int32_t layer, co
                                      const void* k_new, const void* v_new, float gamma,
                                      float softmax_scale, float* out, void* ws, size_t ws_bytes,
                                      hipStream_t stream);
+
+/*
+ * The same decode step (Eq. 5 update included), settled within the call:
+ * items 1-3 of lethe_decode_attn_score, except that the call's own score
+ * update is applied before its work ends in stream order, so afterwards
+ * `score` of the layer is current and no step of it is pending.  Meant for
+ * the last step before a prune round, which then finds nothing to apply and
+ * reads no K row for it.  The step's logits (8 floats per row of the layer)
+ * pass through ws, and a second kernel applies them; the scores equal, bit
+ * for bit, those that lethe_decode_attn_score followed by lethe_score_flush
+ * gives.
+ *  ws  at least lethe_workspace_bytes(cache, LETHE_OP_DECODE_FINAL) bytes:
+ *      the LETHE_OP_DECODE bytes plus about 32 bytes per row of a layer.
+ * Arguments, layouts, skipped sequences (which keep their pending step) and
+ * errors as for lethe_decode_attn_score.
+ */
+lethe_status lethe_decode_attn_score_final(const lethe_cache* cache, int32_t layer, const void* q,
+                                           const void* k_new, const void* v_new, float gamma,
+                                           float softmax_scale, float* out, void* ws, size_t ws_bytes,
+                                           hipStream_t stream);
 
 /*
  * Causal prefill attention that seeds the importance scores, for one layer.

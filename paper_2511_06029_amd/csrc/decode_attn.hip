@@ -279,6 +279,9 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
   const char* Kb = reinterpret_cast<const char*>(a.k) + ck.segrow0 * ROWB;
   const char* Vb = reinterpret_cast<const char*>(a.v) + ck.segrow0 * ROWB;
   float* const sseg = a.score + ck.segrow0;
+  // Settling call: this step's S = Q K^T per row, in the orientation and
+  // arithmetic of the deferred update.
+  float* const xlog = a.logit ? a.logit + ck.segrow0 * kLogitStride : nullptr;
 
   // Loads of a step: K rows into the operand registers and the old scores of
   // rows base + 16 g4 + s (lane groups 0 and 1, used if the pending update
@@ -356,6 +359,17 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
       sacc[T] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) sacc[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], qb[kk], sacc[T], 0, 0, 0);
+    }
+    if (xlog) {
+      // Lane (g4 < 2, s): heads 4 g4 .. 4 g4 + 3 of row 16 T + s, one 16-byte store.
+#pragma unroll
+      for (int T = 0; T < 2; ++T) {
+        f32x4_t sx = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) sx = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qb[kk], kr[T][kk], sx, 0, 0, 0);
+        const int row = base + 16 * T + s;
+        if (g4 < 2 && row < re) *reinterpret_cast<f32x4_t*>(xlog + (long long)row * kLogitStride + 4 * g4) = sx;
+      }
     }
     if (pstep) {
       // S = Q_prev K^T: lane (g4, s) gets heads 4 g4 + rr of row 16 T + s.
@@ -440,6 +454,16 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
           *reinterpret_cast<const uint4*>(vn + 16 * lane);
     }
     if (lane == 0) pd.score[ck.ncache] = 0.0f;
+    if (xlog) {
+      // The appended row's logits as a cached row would give them: every
+      // column of the B operand is k_new.
+      f32x4_t sx = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        sx = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qb[kk], *reinterpret_cast<const bf16x8_t*>(kn + 64 * kk + 16 * g4),
+                                                     sx, 0, 0, 0);
+      if (g4 < 2 && s == 0) *reinterpret_cast<f32x4_t*>(xlog + (long long)ck.ncache * kLogitStride + 4 * g4) = sx;
+    }
     // x_s = scale q_s . k_new: each lane group sums its quarter of the dims.
     float acc = 0.0f;
     const uint32_t* kq = reinterpret_cast<const uint32_t*>(kn);
@@ -555,6 +579,7 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const ReadP
   }
   const float* Kb = reinterpret_cast<const float*>(a.k) + ck.segrow0 * D + dp * EPL;
   const float* Vb = reinterpret_cast<const float*>(a.v) + ck.segrow0 * D + dp * EPL;
+  float* const xlog = a.logit ? a.logit + ck.segrow0 * kLogitStride : nullptr;
 
   auto consume = [&](const uint4* kr, const uint4* vr, const bool* valid, bool pstep, const int* row,
                      const float* sold) {
@@ -570,6 +595,7 @@ __device__ void attn_chunk_f32(const DecodeArgs& a, const Chunk& ck, const ReadP
         for (int e = 0; e < EPL; ++e) acc = fmaf(qf[g][e], kf[e], acc);
         const float xs = group_sum<LPR>(acc);  // every lane takes part
         x[u][g] = valid[u] ? xs : -INFINITY;
+        if (xlog && dp == 0 && valid[u]) xlog[(long long)row[u] * kLogitStride + g] = xs;
       }
       if (pstep) {
         float c = 0.0f;
@@ -721,10 +747,12 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   const bool bad = n < 0 || cp < 0 || n > cp || sbase < 0 || sbase + (long long)a.HK * cp > a.rows_per_layer;
   const bool ovf = !bad && app && n >= cp;
   const int n_att = (bad || ovf) ? 0 : n + (app ? 1 : 0);
+  const bool settle = a.logit != nullptr;
   if (n_att == 0) {
     // Skipped (flagged) or empty sequence: its out rows get NaN or 0, nothing
     // else of it changes, and no counter is touched.
     if (c == 0) {
+      if (settle && h == 0 && tid == 0) a.apply_rows[b] = 0;
       const float fill = (bad || ovf) ? __int_as_float(0x7fc00000) : 0.0f;
       float* ob = a.out + ((long long)b * HQ + (long long)h * G) * D;
       for (int i = tid; i < G * D; i += kThreads) ob[i] = fill;
@@ -777,7 +805,10 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   auto publish = [&](int seen) {
     if (seen != seq_full) return;
     if (app) a.len[b] = n_att;
-    a.pend_len[b] = n_att;
+    // A settling call leaves nothing pending: its second launch applies the
+    // step to the n_att rows.
+    a.pend_len[b] = settle ? 0 : n_att;
+    if (settle) a.apply_rows[b] = n_att;
     a.pend_par[b] = par ^ 1;
     a.pend_gamma[b] = a.gamma;
     a.pend_scale[b] = a.scale_log2;
@@ -992,6 +1023,55 @@ __global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
   }
 }
 
+// Second launch of a settling call: s <- gamma s + sum_g exp2(x_g - M_g) / L_g
+// over the rows each sequence's decode attended, from the logits that launch
+// stored and its (M, 1/L); the deferred update's arithmetic, term for term
+// (bf16: heads 0-3 and 4-7 summed apart, then added).  nb blocks per segment.
+template <typename T, int G>
+__global__ __launch_bounds__(kThreads) void settle_kernel(DecodeArgs a, int nb) {
+  const int segs = a.B * a.HK;
+  const int seg = (int)(blockIdx.x % segs);
+  const int c = (int)(blockIdx.x / segs);
+  const int b = seg / a.HK;
+  const int h = seg - b * a.HK;
+  const int rows = a.apply_rows[b];
+  if (rows <= 0) return;
+  const long long segrow0 = a.seq_base[b] + (long long)h * a.cap[b];
+  const float* st = a.segstat + (long long)seg * 2 * G;
+  float M[G], iL[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    M[g] = st[g];
+    iL[g] = st[G + g];
+  }
+  float* sc = a.score + segrow0;
+  const float* xl = a.logit + segrow0 * kLogitStride;
+  for (int j = c * kThreads + (int)threadIdx.x; j < rows; j += nb * kThreads) {
+    const f32x4_t x0 = *reinterpret_cast<const f32x4_t*>(xl + (long long)j * kLogitStride);
+    const f32x4_t x1 = G > 4 ? *reinterpret_cast<const f32x4_t*>(xl + (long long)j * kLogitStride + 4)
+                             : f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    float add;
+    if constexpr (sizeof(T) == 2) {
+      float lo = 0.0f, hi = 0.0f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float x = g < 4 ? x0[g & 3] : x1[g & 3];
+        const float t = hw_exp2(fmaf(x, a.scale_log2, -M[g]));
+        if (g < 4)
+          lo = fmaf(t, iL[g], lo);
+        else
+          hi = fmaf(t, iL[g], hi);
+      }
+      add = lo + hi;
+    } else {
+      add = 0.0f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) add = fmaf(hw_exp2((g < 4 ? x0[g & 3] : x1[g & 3]) - M[g]), iL[g], add);
+    }
+    sc[j] = fmaf(a.gamma, sc[j], add);
+  }
+}
+
 __global__ void flush_clear_kernel(int32_t* pend_len, int count) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) pend_len[i] = 0;
@@ -1040,6 +1120,15 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   const auto kernel = decode_kernel<T, D, G>();
   hipLaunchKernelGGL(kernel, dim3((unsigned)(segs * nch)), dim3(kThreads), 0, s, a);
   if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
+  if (a.logit) {
+    // About four rows per thread at the average segment capacity.
+    int64_t nb = a.rows_per_layer / segs / (4 * kThreads);
+    if (nb < 1) nb = 1;
+    if (nb > 64) nb = 64;
+    const auto settle = settle_kernel<T, G>;
+    hipLaunchKernelGGL(settle, dim3((unsigned)(segs * nb)), dim3(kThreads), 0, s, a, (int)nb);
+    if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
+  }
   return LETHE_OK;
 }
 

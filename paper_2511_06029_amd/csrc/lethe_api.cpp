@@ -87,6 +87,8 @@ size_t lethe_workspace_bytes(const lethe_cache* c, int op) {
   switch (op) {
     case LETHE_OP_DECODE:
       return decode_ws_bytes(c->num_seqs, c->num_kv_heads, group_size(c), c->head_dim);
+    case LETHE_OP_DECODE_FINAL:
+      return decode_final_ws_bytes(c->num_seqs, c->num_kv_heads, group_size(c), c->head_dim, c->rows_per_layer);
     case LETHE_OP_SPARSITY:
       return 0;
     case LETHE_OP_SELECT:
@@ -108,10 +110,13 @@ lethe_status lethe_score_flush(const lethe_cache* c, hipStream_t stream) {
   return flush_pending(c, stream);
 }
 
-lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const void* q,
-                                     const void* k_new, const void* v_new, float gamma,
-                                     float softmax_scale, float* out, void* ws, size_t ws_bytes,
-                                     hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+lethe_status decode_call(const lethe_cache* c, int32_t layer, const void* q, const void* k_new,
+                         const void* v_new, float gamma, float softmax_scale, float* out, void* ws,
+                         size_t ws_bytes, bool settle, hipStream_t stream) {
   lethe_status st = check_cache(c);
   if (st != LETHE_OK) return st;
   if (layer < 0 || layer >= c->num_layers) return LETHE_ERR_INVALID;
@@ -121,7 +126,9 @@ lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const 
   if (isnan(softmax_scale) || isinf(softmax_scale)) return LETHE_ERR_INVALID;
   const int G = group_size(c);
   const int D = c->head_dim;
-  if (ws_bytes < decode_ws_bytes(c->num_seqs, c->num_kv_heads, G, D)) return LETHE_ERR_WORKSPACE;
+  const size_t need = settle ? decode_final_ws_bytes(c->num_seqs, c->num_kv_heads, G, D, c->rows_per_layer)
+                             : decode_ws_bytes(c->num_seqs, c->num_kv_heads, G, D);
+  if (ws_bytes < need) return LETHE_ERR_WORKSPACE;
   float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)D);
 
   const size_t eb = elem_bytes(c->dtype);
@@ -159,7 +166,27 @@ lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const 
   a.dev_status = c->dev_status;
   a.nch = 0;  // chosen by the launcher
   a.deterministic = 0;
+  a.logit = settle ? (float*)((char*)ws + decode_final_logit_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
+  a.apply_rows = settle ? (int32_t*)((char*)ws + decode_final_rows_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
   return launch_decode(a, c->dtype, D, G, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const void* q,
+                                     const void* k_new, const void* v_new, float gamma,
+                                     float softmax_scale, float* out, void* ws, size_t ws_bytes,
+                                     hipStream_t stream) {
+  return decode_call(c, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, ws_bytes, false, stream);
+}
+
+lethe_status lethe_decode_attn_score_final(const lethe_cache* c, int32_t layer, const void* q,
+                                           const void* k_new, const void* v_new, float gamma,
+                                           float softmax_scale, float* out, void* ws, size_t ws_bytes,
+                                           hipStream_t stream) {
+  return decode_call(c, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, ws_bytes, true, stream);
 }
 
 lethe_status lethe_layer_sparsity(const lethe_cache* c, const int64_t* global_budget,

@@ -82,6 +82,18 @@ inline size_t decode_ws_bytes(int B, int HK, int G, int D) {
   return align_up((size_t)decode_max_chunks(B, HK) * part_stride(G, D) * sizeof(float), 256);
 }
 
+// A decode call that settles its own score update also keeps, after the
+// partials, the rows to update per sequence and every row's logits of the
+// step: 8 floats per row of the layer (query heads of the group, padded).
+constexpr int kLogitStride = 8;
+inline size_t decode_final_rows_off(int B, int HK, int G, int D) { return decode_ws_bytes(B, HK, G, D); }
+inline size_t decode_final_logit_off(int B, int HK, int G, int D) {
+  return decode_final_rows_off(B, HK, G, D) + align_up((size_t)B * sizeof(int32_t), 256);
+}
+inline size_t decode_final_ws_bytes(int B, int HK, int G, int D, int64_t rows_per_layer) {
+  return decode_final_logit_off(B, HK, G, D) + align_up((size_t)rows_per_layer * kLogitStride * sizeof(float), 256);
+}
+
 struct DecodeArgs {
   const void* k;         // layer base, rows x D of the storage type
   const void* v;
@@ -111,6 +123,11 @@ struct DecodeArgs {
   int32_t* dev_status;
   int32_t nch;           // blocks per segment, 1 .. kMaxChunksPerSeg
   int32_t deterministic; // fixed step schedule instead of the step counter
+  // Settling call only (else null): the step's logits [rows_per_layer][8]
+  // (raw q.k for bf16, scaled to log2 units for fp32) and the rows to
+  // update per sequence (0: skipped), both in the workspace.
+  float* logit;
+  int32_t* apply_rows;
 };
 
 struct FlushArgs {

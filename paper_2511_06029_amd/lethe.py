@@ -14,11 +14,11 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblethe.so
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
 DEV_APPEND_OVERFLOW, DEV_INFEASIBLE, DEV_BAD_LAYOUT, DEV_HEAD_MISMATCH = 1, 2, 4, 8
-OP_DECODE, OP_SPARSITY, OP_SELECT, OP_COMPACT = 0, 1, 2, 3
+OP_DECODE, OP_SPARSITY, OP_SELECT, OP_COMPACT, OP_DECODE_FINAL = 0, 1, 2, 3, 4
 
 SHRINK_NO_BREAKPOINT, SHRINK_NOT_TRIGGERED = -1, -2
 
-EXPORTED = ("lethe_workspace_bytes", "lethe_state_bytes", "lethe_decode_attn_score",
+EXPORTED = ("lethe_workspace_bytes", "lethe_state_bytes", "lethe_decode_attn_score", "lethe_decode_attn_score_final",
             "lethe_layer_sparsity", "lethe_rasr_select", "lethe_rasr_select_shared",
             "lethe_segmented_shrink", "lethe_kv_compact", "lethe_score_flush",
             "lethe_prefill_attn_score", "lethe_prefill_workspace_bytes", "lethe_status_string")
@@ -63,6 +63,8 @@ def load():
         lib.lethe_score_flush.restype = ctypes.c_int
         lib.lethe_decode_attn_score.argtypes = [pc, i32, vp, vp, vp, ctypes.c_float, ctypes.c_float, vp, vp, sz, vp]
         lib.lethe_decode_attn_score.restype = ctypes.c_int
+        lib.lethe_decode_attn_score_final.argtypes = lib.lethe_decode_attn_score.argtypes
+        lib.lethe_decode_attn_score_final.restype = ctypes.c_int
         lib.lethe_layer_sparsity.argtypes = [pc, vp, i32, i32, vp, vp, vp, vp, sz, vp]
         lib.lethe_layer_sparsity.restype = ctypes.c_int
         lib.lethe_rasr_select.argtypes = [pc, vp, i32, i32, vp, vp, sz, vp]
@@ -127,6 +129,16 @@ def decode_attn_score(cache, layer, q, k_new, v_new, gamma, softmax_scale, out, 
                                         _p(v_new), float(gamma), float(softmax_scale), _p(out), _p(ws),
                                         ws.numel() * ws.element_size(), _stream(stream))
     _check("lethe_decode_attn_score", st)
+
+
+def decode_attn_score_final(cache, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, stream=None):
+    """lethe_decode_attn_score_final: the same step with its own score update
+    applied within the call (nothing left pending); ws sized for
+    OP_DECODE_FINAL."""
+    st = load().lethe_decode_attn_score_final(ctypes.byref(cache.c_struct()), int(layer), _p(q), _p(k_new),
+                                              _p(v_new), float(gamma), float(softmax_scale), _p(out), _p(ws),
+                                              ws.numel() * ws.element_size(), _stream(stream))
+    _check("lethe_decode_attn_score_final", st)
 
 
 def layer_sparsity(cache, global_budget, recent, sink, sparsity_in, sparsity_out, budget_out,

@@ -35,11 +35,12 @@ def make(**kw):
     return c
 
 
-def decode(c, layer=0, q=FAKE, kn=FAKE, vn=FAKE, gamma=0.9, scale=0.0, out=FAKE, ws=FAKE, wsb=None):
+def decode(c, layer=0, q=FAKE, kn=FAKE, vn=FAKE, gamma=0.9, scale=0.0, out=FAKE, ws=FAKE, wsb=None, final=False):
     lib = L.load()
     if wsb is None:
-        wsb = lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_DECODE) if L.load() else 0
-    return lib.lethe_decode_attn_score(ctypes.byref(c), layer, q, kn, vn, gamma, scale, out, ws, wsb, None)
+        wsb = lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_DECODE_FINAL if final else L.OP_DECODE)
+    fn = lib.lethe_decode_attn_score_final if final else lib.lethe_decode_attn_score
+    return fn(ctypes.byref(c), layer, q, kn, vn, gamma, scale, out, ws, wsb, None)
 
 
 def test_status_strings():
@@ -58,6 +59,10 @@ def test_workspace_sizes():
     assert w % 256 == 0
     # device pointers are not looked at
     assert lib.lethe_workspace_bytes(ctypes.byref(make(k=None, state=None)), L.OP_DECODE) == w
+    # settling call: the partials, B row counts and 8 floats per row of a layer
+    wf = lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_DECODE_FINAL)
+    assert wf >= w + B * 4 + 4096 * 8 * 4 and wf % 256 == 0
+    assert lib.lethe_workspace_bytes(ctypes.byref(make(rows_per_layer=8192)), L.OP_DECODE_FINAL) == wf + 4096 * 8 * 4
     assert lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_COMPACT) >= 2 * B * HK * 4
     assert lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_SELECT) == 0
     assert lib.lethe_workspace_bytes(ctypes.byref(c), 99) == 0
@@ -79,6 +84,7 @@ def test_workspace_sizes():
 def test_cache_validation(field, value, want):
     c = make(**{field: value})
     assert decode(c, wsb=1 << 40) == want
+    assert decode(c, wsb=1 << 40, final=True) == want
     lib = L.load()
     assert lib.lethe_rasr_select(ctypes.byref(c), FAKE, 8, 0, FAKE, None, 0, None) == want
     assert lib.lethe_rasr_select_shared(ctypes.byref(c), FAKE, 8, 0, FAKE, None, 0, None) == want
@@ -87,23 +93,27 @@ def test_cache_validation(field, value, want):
     assert lib.lethe_layer_sparsity(ctypes.byref(c), FAKE, 8, 0, None, FAKE, FAKE, None, 0, None) == want
 
 
-def test_decode_argument_validation():
+@pytest.mark.parametrize("final", [False, True])
+def test_decode_argument_validation(final):
     c = make()
-    assert decode(c, layer=-1) == L.ERR_INVALID
-    assert decode(c, layer=2) == L.ERR_INVALID
-    assert decode(c, q=None) == L.ERR_INVALID
-    assert decode(c, out=None) == L.ERR_INVALID
-    assert decode(c, ws=None) == L.ERR_INVALID
-    assert decode(c, kn=None) == L.ERR_INVALID          # v_new without k_new
-    assert decode(c, vn=None) == L.ERR_INVALID
+    assert decode(c, layer=-1, final=final) == L.ERR_INVALID
+    assert decode(c, layer=2, final=final) == L.ERR_INVALID
+    assert decode(c, q=None, final=final) == L.ERR_INVALID
+    assert decode(c, out=None, final=final) == L.ERR_INVALID
+    assert decode(c, ws=None, final=final) == L.ERR_INVALID
+    assert decode(c, kn=None, final=final) == L.ERR_INVALID          # v_new without k_new
+    assert decode(c, vn=None, final=final) == L.ERR_INVALID
     for g in (0.0, -0.5, 1.0001, math.nan, math.inf):
-        assert decode(c, gamma=g) == L.ERR_INVALID
+        assert decode(c, gamma=g, final=final) == L.ERR_INVALID
     for s in (math.nan, math.inf, -math.inf):
-        assert decode(c, scale=s) == L.ERR_INVALID
+        assert decode(c, scale=s, final=final) == L.ERR_INVALID
     lib = L.load()
-    need = lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_DECODE)
-    assert decode(c, wsb=need - 1) == L.ERR_WORKSPACE
-    assert decode(c, wsb=0) == L.ERR_WORKSPACE
+    need = lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_DECODE_FINAL if final else L.OP_DECODE)
+    assert decode(c, wsb=need - 1, final=final) == L.ERR_WORKSPACE
+    assert decode(c, wsb=0, final=final) == L.ERR_WORKSPACE
+    if final:
+        # the deferred call's workspace is too small for the settling one
+        assert decode(c, wsb=lib.lethe_workspace_bytes(ctypes.byref(c), L.OP_DECODE), final=True) == L.ERR_WORKSPACE
 
 
 def test_prune_argument_validation():
