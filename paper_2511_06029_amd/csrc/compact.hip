@@ -1,8 +1,9 @@
 // In-place, order-preserving compaction of K, V and score rows, gfx950.
 //
 // One block per (layer, sequence, KV head) segment.  Rows before the first
-// evicted row stay where they are.  From there the block sweeps the source rows
-// in tiles of 128: two wavefronts ballot the keep flags of the tile and list
+// evicted row (found with 16 independent flag loads per thread) stay where
+// they are.  From there the block sweeps the source rows in tiles of 256:
+// four wavefronts ballot the keep flags of the tile and list
 // the kept rows' source indices in LDS; every thread loads its share of those
 // rows (16 bytes per lane) into registers, waits for its loads, the block
 // synchronises, and the rows are stored to their destinations (a running
@@ -18,8 +19,8 @@ namespace lethe {
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kTile = 128;
+constexpr int kThreads = 512;
+constexpr int kTile = 256;
 constexpr int kTileWaves = kTile / kWave;
 // 16 bytes of a row; a vector type, so arrays of them stay in registers.
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
@@ -55,19 +56,28 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   __shared__ int s_first;
   __shared__ int s_src[kTile];          // per ballot wave: its kept rows in order
   __shared__ int s_cnt[kTileWaves];
+  // 16 independent flag loads per thread and round; the lowest evicted row
+  // of the round wins.
   if (tid == 0) s_first = n;
   __syncthreads();
-  {
+  int first = n;
+  for (int c0 = 0; c0 < n; c0 += 16 * kThreads) {
+    // Clamped, unconditional loads, all issued before the first is used.
+    uint8_t kv[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) kv[k] = keep[min(c0 + k * kThreads + tid, n - 1)];
     int f = n;
-    for (int j = tid; j < n; j += kThreads)
-      if (keep[j] == 0) {
-        f = j;
-        break;
-      }
+#pragma unroll
+    for (int k = 15; k >= 0; --k) {
+      const int j = c0 + k * kThreads + tid;
+      if (j < n && kv[k] == 0) f = j;
+    }
     if (f < n) atomicMin(&s_first, f);
+    __syncthreads();
+    first = s_first;
+    __syncthreads();  // every thread has read s_first before it can change again
+    if (first < n) break;
   }
-  __syncthreads();
-  const int first = s_first;
   int pos = first;  // next destination row
   const int lane = tid & (kWave - 1);
   const int w = tid / kWave;

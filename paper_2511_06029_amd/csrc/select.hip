@@ -17,9 +17,11 @@
 // Selection: fp32 keys map to 32-bit words whose unsigned order is the float
 // order (+0 and -0 equal, NaN below every number).  An MSB-first radix select
 // with 8-bit digits and a 256-bin LDS histogram finds the exact key T of the
-// m-th best candidate and how many candidates equal to T are still needed; an
-// ordered pass keeps every candidate above T and the lowest-indexed ones
-// equal to T.
+// m-th best candidate, how many candidates equal to T are still needed and
+// how many there are.  When all of them are needed (the usual case) one
+// elementwise pass keeps the candidates at or above T; otherwise an ordered
+// pass keeps every candidate above T and the lowest-indexed ones equal to T.
+// Each thread issues the loads of eight rows before it uses the first.
 #include "device_common.h"
 #include "lethe_internal.h"
 
@@ -55,6 +57,22 @@ struct Scores {
       return acc;
     }
   }
+  // The same for rows j[0 .. U) (valid indices): each head's loads of the U
+  // rows are issued together, unconditionally.
+  template <int U>
+  __device__ inline void batch(const int* j, float* v) const {
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = s[j[u]];
+    if constexpr (kShared) {
+      for (int h = 1; h < heads; ++h) {
+        float x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[u] = s[h * hstride + j[u]];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = v[u] + x[u];
+      }
+    }
+  }
 };
 
 template <int NT>
@@ -68,19 +86,32 @@ struct SelectShared {
   int plan[4];  // lo, hi, m, keep-all flag
 };
 
-// Key T of the m-th best key among rows [lo, hi) (m >= 1) and how many rows
-// with key T belong to the best m.  All threads get both.
+// Rows a thread loads before it uses the first of them (the passes are bound
+// by load latency).
+constexpr int kU = 8;
+
+// Key T of the m-th best key among rows [lo, hi) (m >= 1), how many rows
+// with key T belong to the best m, and how many rows have key T.  All
+// threads get the three.
 template <int NT, class KeyFn>
 __device__ void radix_select(const KeyFn& rank, int lo, int hi, uint32_t m, SelectShared<NT>& sh,
-                             uint32_t* T_out, uint32_t* need_out) {
+                             uint32_t* T_out, uint32_t* need_out, uint32_t* count_out) {
   const int tid = threadIdx.x;
-  uint32_t prefix = 0, pmask = 0, need = m;
+  uint32_t prefix = 0, pmask = 0, need = m, count = 0;
   for (int shift = 24; shift >= 0; shift -= 8) {
     if (tid < 256) sh.hist[tid] = 0;
     __syncthreads();
-    for (int j = lo + tid; j < hi; j += NT) {
-      const uint32_t key = order_key(rank(j));
-      if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
+    for (int j0 = lo; j0 < hi; j0 += kU * NT) {
+      int jj[kU];
+      float v[kU];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) jj[u] = min(j0 + u * NT + tid, hi - 1);
+      rank.template batch<kU>(jj, v);
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const uint32_t key = order_key(v[u]);
+        if (j0 + u * NT + tid < hi && (key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
+      }
     }
     __syncthreads();
     // suffix[d] = matching keys whose digit is >= d: wave 0, four bins a lane.
@@ -109,10 +140,12 @@ __device__ void radix_select(const KeyFn& rank, int lo, int hi, uint32_t m, Sele
     prefix |= sh.digit << shift;
     pmask |= 255u << shift;
     need = sh.need;
+    count = sh.hist[sh.digit];
     __syncthreads();
   }
   *T_out = prefix;
   *need_out = need;
+  *count_out = count;
 }
 
 // Block-wide max of a key and sum of a count; every thread gets both.
@@ -242,8 +275,31 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
       for (int j = tid; j < n; j += NT) keep[(long long)hh * c + j] = 1;
     return;
   }
-  uint32_t T = 0, need = 0;
-  if (m > 0) radix_select<NT>(rank, lo, hi, (uint32_t)m, sh, &T, &need);
+  uint32_t T = 0, need = 0, countT = 0;
+  if (m > 0) radix_select<NT>(rank, lo, hi, (uint32_t)m, sh, &T, &need, &countT);
+  if (m == 0 || need == countT) {
+    // Every candidate with key T is kept (or none is a candidate to keep):
+    // no tie to break, so each row is decided on its own.
+    for (int j0 = 0; j0 < n; j0 += kU * NT) {
+      float v[kU];
+      if (m > 0) {
+        int jj[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) jj[u] = min(max(j0 + u * NT + tid, lo), hi - 1);
+        rank.template batch<kU>(jj, v);
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int j = j0 + u * NT + tid;
+        if (j < n) {
+          const bool cand = m > 0 && j >= lo && j < hi;
+          const uint8_t kp = (j < fs || j >= fr || (cand && order_key(v[u]) >= T)) ? 1 : 0;
+          for (int hh = 0; hh < nheads; ++hh) keep[(long long)hh * c + j] = kp;
+        }
+      }
+    }
+    return;
+  }
   // Ordered pass: ties with key T are taken by increasing row index.
   long long carry = 0;
   for (int j0 = 0; j0 < n; j0 += NT) {

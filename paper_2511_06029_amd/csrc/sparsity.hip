@@ -4,7 +4,8 @@
 // hoyer_kernel: one block per (sequence b, layer l).  Streams the H_KV score
 // vectors of the live rows once (4 bytes per row), forms a_j = sum_h s_h,j in
 // fp64, and reduces |a|_1 and |a|_2^2 in fp64 (the score vectors of a layer can
-// hold 10^5 rows of widely varying magnitude).
+// hold 10^5 rows of widely varying magnitude).  The loads of eight rows of up
+// to four heads are issued together: the kernel is bound by load latency.
 // budget_kernel: one wavefront per sequence runs the split, a lane per layer
 // (up to four layers a lane for L <= 256).
 #include <math.h>
@@ -34,12 +35,37 @@ __global__ __launch_bounds__(kThreads) void hoyer_kernel(SparsityArgs a) {
     return;
   }
   const float* s0 = a.score + (long long)l * a.rows_per_layer + base;
+  // Rows tid, tid + kThreads, ... in order; kU rows and up to four heads of
+  // loads in flight per thread before the first use.
+  constexpr int kU = 8;
   double l1 = 0.0, l2 = 0.0;
-  for (int j = tid; j < n; j += kThreads) {
-    double aj = 0.0;
-    for (int h = 0; h < a.HK; ++h) aj += (double)s0[(long long)h * c + j];
-    l1 += fabs(aj);
-    l2 += aj * aj;
+  for (int j0 = 0; j0 < n; j0 += kU * kThreads) {
+    double aj[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) aj[u] = 0.0;
+    for (int h0 = 0; h0 < a.HK; h0 += 4) {
+      // Clamped, unconditional loads (a guarded load would be waited for
+      // inside its own branch); the values past the ends are not used.
+      float x[4][kU];
+#pragma unroll
+      for (int hh = 0; hh < 4; ++hh)
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          const int j = min(j0 + u * kThreads + tid, n - 1);
+          x[hh][u] = s0[(long long)min(h0 + hh, a.HK - 1) * c + j];
+        }
+#pragma unroll
+      for (int hh = 0; hh < 4; ++hh)
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+          if (h0 + hh < a.HK) aj[u] += (double)x[hh][u];
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (j0 + u * kThreads + tid < n) {
+        l1 += fabs(aj[u]);
+        l2 += aj[u] * aj[u];
+      }
   }
   __shared__ double red[2][kThreads / kWave];
   l1 = wave_sum_d(l1);
