@@ -1078,8 +1078,10 @@ __global__ void flush_clear_kernel(int32_t* pend_len, int count) {
 }
 
 // Overrides read at every call: LETHE_DECODE_BLOCKS (blocks to aim for per
-// launch; default two per CU) and LETHE_DECODE_DETERMINISTIC (non-zero: fixed
-// step schedule, so repeated calls give bit-identical results).
+// launch; default two per CU and at least four per segment) and
+// LETHE_DECODE_DETERMINISTIC (non-zero: fixed step schedule, so repeated
+// calls give bit-identical results).
+constexpr int64_t kMinChunksPerSeg = 4;
 int env_int(const char* name) {
   const char* v = getenv(name);
   return v ? atoi(v) : 0;
@@ -1112,6 +1114,10 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   a.deterministic = env_int("LETHE_DECODE_DETERMINISTIC") != 0;
   const int64_t segs = (int64_t)a.B * a.HK;
   int64_t nch = target / segs;
+  // At least four blocks per segment: with many segments of ragged lengths
+  // the blocks outnumber the resident slots, and the dispatcher hands the
+  // slots of early finishers to the waiting blocks.
+  if (env_blocks <= 0 && nch < kMinChunksPerSeg) nch = kMinChunksPerSeg;
   const int64_t cap_nch = decode_max_chunks(a.B, a.HK) / segs;
   if (nch > cap_nch) nch = cap_nch;
   if (nch > kMaxChunksPerSeg) nch = kMaxChunksPerSeg;
