@@ -393,6 +393,8 @@ def run_prefill(args):
     cfg = CONFIGS[2]
     dev = "cuda"
     torch.cuda.set_device(0)
+    if args.steps is None:
+        args.steps = 10  # prefills of all 32 layers
     Lyr, B, HQ, HK, D, T = cfg.num_layers, cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.prompt
     log("allocating cache: %d layers x %d seqs x %d kv heads x %d rows" % (Lyr, B, HK, T))
     cache = L.LetheCache(Lyr, [T] * B, HQ, HK, D, dtype="bf16", device=dev)
