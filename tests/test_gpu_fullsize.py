@@ -4,7 +4,8 @@ For each of the Llama-8B / Qwen-7B workloads (batch, KV heads, head_dim and
 the full cached lengths of one layer: 2k, 16k, U[8k, 32k], logU[1k, 64k]) a
 two-layer cache is filled by the seeded Zipf generator and driven through
 the library with its default launch configuration (the one bench.py times):
-two decode steps with append, then a prune round.  The oracle recomputes a
+two decode steps with append, the second one the settling call that bench.py
+ends each interval with, then a prune round.  The oracle recomputes a
 sample of segments one by one (the shortest and longest sequences and a few
 seeded picks):
 
@@ -14,8 +15,8 @@ seeded picks):
 * keep masks and compacted K / V / score rows bit-exact given the device's
   scores.
 
-Configs with 512 or more segments per layer run one chunk per segment; the
-others split segments across blocks, so both decode paths are covered.
+The default launch splits every segment over at least four blocks (the
+one-block path is covered by the LETHE_DECODE_BLOCKS=1 parity tests).
 """
 import math
 import sys
@@ -86,7 +87,7 @@ def test_fullsize_decode_and_prune(cfg_id):
                 c.v[l, s0:s0 + int(T[b])] = V[h]
             del K, V
     c.len.copy_(torch.from_numpy(np.tile(T.astype(np.int32), (LAYERS, 1))).to(DEV))
-    ws = c.workspace(L.OP_DECODE)
+    ws = c.workspace(L.OP_DECODE_FINAL)
     torch.cuda.synchronize()
 
     picks = sample_seqs(T)
@@ -104,7 +105,8 @@ def test_fullsize_decode_and_prune(cfg_id):
         for l in range(LAYERS):
             q, kn, vn = gen.step(t, l, T=T + t)
             out = torch.empty((B, HQ, D), dtype=torch.float32, device=DEV)
-            L.decode_attn_score(c, l, q, kn, vn, cfg.gamma, 0.0, out, ws)
+            fn = L.decode_attn_score_final if t == STEPS - 1 else L.decode_attn_score
+            fn(c, l, q, kn, vn, cfg.gamma, 0.0, out, ws)
             torch.cuda.synchronize()
             og, qh, kh, vh = f32(out), f32(q), f32(kn), f32(vn)
             for b in picks:
@@ -118,8 +120,7 @@ def test_fullsize_decode_and_prune(cfg_id):
                     close(og[b, h * G:(h + 1) * G], o, "cfg%d out step %d l%d b%d h%d" % (cfg_id, t, l, b, h))
     assert int(c.dev_status[0]) == 0
     assert (c.len.cpu().numpy() == (T + STEPS).astype(np.int32)[None]).all()
-    c.flush()
-    torch.cuda.synchronize()
+    # The settling call left nothing pending: the scores are current as they are.
     for (l, b, h), (K, V, s) in ref.items():
         s0, _ = c.seg_rows(b, h)
         close(f32(c.score[l, s0:s0 + K.shape[0]]), s, "cfg%d scores l%d b%d h%d" % (cfg_id, l, b, h))
