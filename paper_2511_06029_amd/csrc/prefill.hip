@@ -441,31 +441,47 @@ __global__ __launch_bounds__(kPfThreads) void prefill_score_kernel(PrefillArgs a
     // No masking when every key is live and precedes every (live) query.
     const bool full = j0w + kPfKeysPerWave - 1 <= pos0 && kPfItemQ * (it + 1) <= sq.qlen &&
                       j0w + kPfKeysPerWave <= sq.n;
+    constexpr int QH = kPfItemQ / 16;
+    // Both query halves' operands and statistics, then every MFMA of the
+    // item with the k-step outermost: QH * 4 independent accumulators.
+    pf_bf16x8_t qv[QH][KK];
+    float off[QH];
 #pragma unroll
-    for (int qh = 0; qh < kPfItemQ / 16; ++qh) {
-      pf_bf16x8_t qv[KK];
+    for (int qh = 0; qh < QH; ++qh) {
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
-        qv[kk] = *reinterpret_cast<const pf_bf16x8_t*>(qt + 16 * Cfg::kslot(16 * qh + s, 4 * kk + g4));
+        qv[qh][kk] = *reinterpret_cast<const pf_bf16x8_t*>(qt + 16 * Cfg::kslot(16 * qh + s, 4 * kk + g4));
       // exp2(x - max) / sum = exp2(x - (max + log2(sum))).
       const float2 st = lds_read_f2((const pf_lds_char_t*)(stl + 2 * (16 * qh + s)));
-      const float off = st.x - __log2f(st.y);
+      off[qh] = st.x - __log2f(st.y);
+    }
+    pf_f32x4_t sacc[QH][4];
+#pragma unroll
+    for (int qh = 0; qh < QH; ++qh)
+#pragma unroll
+      for (int T = 0; T < 4; ++T) sacc[qh][T] = pf_f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int qh = 0; qh < QH; ++qh)
+#pragma unroll
+        for (int T = 0; T < 4; ++T)
+          sacc[qh][T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], qv[qh][kk], sacc[qh][T], 0, 0, 0);
+#pragma unroll
+    for (int qh = 0; qh < QH; ++qh) {
       const int i = kPfItemQ * it + 16 * qh + s;
       const int pos = sq.first + i;
       const bool valid = i < sq.qlen;
 #pragma unroll
       for (int T = 0; T < 4; ++T) {
-        pf_f32x4_t sacc = pf_f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[T][kk], qv[kk], sacc, 0, 0, 0);
         if (full) {
 #pragma unroll
-          for (int rr = 0; rr < 4; ++rr) acc[T][rr] += hw_exp2(fmaf(sacc[rr], sc, -off));
+          for (int rr = 0; rr < 4; ++rr) acc[T][rr] += hw_exp2(fmaf(sacc[qh][T][rr], sc, -off[qh]));
         } else {
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
             const int key = j0w + 16 * T + 4 * g4 + rr;
-            const float p = hw_exp2(fmaf(sacc[rr], sc, -off));
+            const float p = hw_exp2(fmaf(sacc[qh][T][rr], sc, -off[qh]));
             acc[T][rr] += (valid && key <= pos && key < sq.n) ? p : 0.0f;
           }
         }
