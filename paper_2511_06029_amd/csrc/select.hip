@@ -21,7 +21,10 @@
 // how many there are.  When all of them are needed (the usual case) one
 // elementwise pass keeps the candidates at or above T; otherwise an ordered
 // pass keeps every candidate above T and the lowest-indexed ones equal to T.
-// Each thread issues the loads of eight rows before it uses the first.
+// Candidate sets of up to kRegKeys rows per thread are read once into
+// registers, and the radix passes and the elementwise pass use those; larger
+// sets are re-read per pass, each thread issuing the loads of eight rows
+// before it uses the first.
 #include "device_common.h"
 #include "lethe_internal.h"
 
@@ -120,6 +123,58 @@ __device__ void radix_select(const KeyFn& rank, int lo, int hi, uint32_t m, Sele
       const uint32_t h2 = sh.hist[4 * tid + 2], h3 = sh.hist[4 * tid + 3];
       const uint32_t tot = h0 + h1 + h2 + h3;
       uint32_t incl = tot;  // sum over lanes tid .. 63
+      for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t v = __shfl_down(incl, o);
+        if (tid + o < kWave) incl += v;
+      }
+      const uint32_t above = incl - tot;
+      sh.suffix[4 * tid + 3] = above + h3;
+      sh.suffix[4 * tid + 2] = above + h3 + h2;
+      sh.suffix[4 * tid + 1] = above + h3 + h2 + h1;
+      sh.suffix[4 * tid] = incl;
+      if (tid == 0) sh.suffix[256] = 0;
+    }
+    __syncthreads();
+    if (tid < 256 && sh.suffix[tid] >= need && sh.suffix[tid + 1] < need) {
+      sh.digit = (uint32_t)tid;
+      sh.need = need - sh.suffix[tid + 1];
+    }
+    __syncthreads();
+    prefix |= sh.digit << shift;
+    pmask |= 255u << shift;
+    need = sh.need;
+    count = sh.hist[sh.digit];
+    __syncthreads();
+  }
+  *T_out = prefix;
+  *need_out = need;
+  *count_out = count;
+}
+
+// Keys a thread keeps in registers: candidate sets of up to kRegKeys * NT rows
+// are read from memory once.
+constexpr int kRegKeys = 32;
+
+// radix_select over keys held in registers: thread t holds the keys of
+// candidates t, t + NT, ... (key[u] for u < cnt; cnt is the same for all
+// threads, slots past the candidates hold 0 and are not counted).
+template <int NT>
+__device__ void radix_select_regs(const uint32_t (&key)[kRegKeys], const bool (&valid)[kRegKeys], uint32_t m,
+                                  SelectShared<NT>& sh, uint32_t* T_out, uint32_t* need_out, uint32_t* count_out) {
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0, pmask = 0, need = m, count = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    if (tid < 256) sh.hist[tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kRegKeys; ++u)
+      if (valid[u] && (key[u] & pmask) == prefix) atomicAdd(&sh.hist[(key[u] >> shift) & 255u], 1u);
+    __syncthreads();
+    if (tid < kWave) {
+      const uint32_t h0 = sh.hist[4 * tid], h1 = sh.hist[4 * tid + 1];
+      const uint32_t h2 = sh.hist[4 * tid + 2], h3 = sh.hist[4 * tid + 3];
+      const uint32_t tot = h0 + h1 + h2 + h3;
+      uint32_t incl = tot;
       for (int o = 1; o < kWave; o <<= 1) {
         const uint32_t v = __shfl_down(incl, o);
         if (tid + o < kWave) incl += v;
@@ -276,7 +331,52 @@ __global__ __launch_bounds__(NT) void select_kernel(SelectArgs a) {
     return;
   }
   uint32_t T = 0, need = 0, countT = 0;
-  if (m > 0) radix_select<NT>(rank, lo, hi, (uint32_t)m, sh, &T, &need, &countT);
+  if (m > 0 && hi - lo <= kRegKeys * NT) {
+    // The candidates' keys in registers, read once (eight rows' loads at a
+    // time); the radix passes and the keep pass use them.
+    uint32_t key[kRegKeys];
+    bool valid[kRegKeys];
+#pragma unroll
+    for (int u0 = 0; u0 < kRegKeys; u0 += kU) {
+      if (lo + u0 * NT < hi) {  // block-uniform
+        int jj[kU];
+        float v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) jj[u] = min(lo + (u0 + u) * NT + tid, hi - 1);
+        rank.template batch<kU>(jj, v);
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          valid[u0 + u] = lo + (u0 + u) * NT + tid < hi;
+          key[u0 + u] = order_key(v[u]);
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          valid[u0 + u] = false;
+          key[u0 + u] = 0u;
+        }
+      }
+    }
+    radix_select_regs<NT>(key, valid, (uint32_t)m, sh, &T, &need, &countT);
+    if (need == countT) {
+      // Forced rows, then every candidate at or above T.
+      for (int j = tid; j < fs; j += NT)
+        for (int hh = 0; hh < nheads; ++hh) keep[(long long)hh * c + j] = 1;
+      for (int j = max(fr, hi) + tid; j < n; j += NT)
+        for (int hh = 0; hh < nheads; ++hh) keep[(long long)hh * c + j] = 1;
+#pragma unroll
+      for (int u = 0; u < kRegKeys; ++u) {
+        const int j = lo + u * NT + tid;
+        if (valid[u]) {
+          const uint8_t kp = (j < fs || j >= fr || key[u] >= T) ? 1 : 0;
+          for (int hh = 0; hh < nheads; ++hh) keep[(long long)hh * c + j] = kp;
+        }
+      }
+      return;
+    }
+  } else if (m > 0) {
+    radix_select<NT>(rank, lo, hi, (uint32_t)m, sh, &T, &need, &countT);
+  }
   if (m == 0 || need == countT) {
     // Every candidate with key T is kept (or none is a candidate to keep):
     // no tie to break, so each row is decided on its own.
