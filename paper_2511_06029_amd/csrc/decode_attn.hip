@@ -877,19 +877,26 @@ constexpr auto decode_kernel() {
 
 // ---------------------------------------------------------------------------
 // Flush: apply the pending step of every (layer, sequence), block per
-// (layer, sequence, KV head); a second kernel clears the pending lengths.
+// (layer, sequence, KV head); the last block of each (layer, sequence)
+// clears its pending length.
 // ---------------------------------------------------------------------------
+// Every flush block of a (layer, sequence) with a pending step counts itself
+// once all its threads are done with the pending state; the last of the H_KV
+// blocks clears the pending length and the counter (which the decode state
+// holds at zero between flushes).
+__device__ inline void flush_done(const FlushArgs& a, int lb) {
+  __syncthreads();
+  if (threadIdx.x == 0 && atomicAdd(&a.flush_cnt[lb], 1) == a.HK - 1) {
+    a.pend_len[lb] = 0;
+    a.flush_cnt[lb] = 0;
+  }
+}
+
 template <typename T, int D, int G>
-__global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
+__device__ void flush_segment_valu(const FlushArgs& a, int lb, int h, int l, int b, int P) {
   constexpr int EPL = Elem<T>::kPer16B;
   constexpr int LPR = D / EPL;
   constexpr int RPW = kWave / LPR;
-  const int lb = blockIdx.x / a.HK;
-  const int h = blockIdx.x - lb * a.HK;
-  const int l = lb / a.B;
-  const int b = lb - l * a.B;
-  const int P = a.pend_len[lb];
-  if (P <= 0) return;
   const int n = a.len[lb];
   const int cp = a.cap[b];
   const long long sbase = a.seq_base[b];
@@ -934,22 +941,26 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
   }
 }
 
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
+  const int lb = blockIdx.x / a.HK;
+  const int h = blockIdx.x - lb * a.HK;
+  const int P = a.pend_len[lb];
+  if (P <= 0) return;
+  flush_segment_valu<T, D, G>(a, lb, h, lb / a.B, lb % a.B, P);
+  flush_done(a, lb);
+}
+
 // bf16 flush on the matrix cores, the pending-update half of the decode
 // loop on its own: one block per (layer, sequence, KV head); wave w takes the
 // 32-row steps w, w + 4, ...; each step's K rows load straight into the
 // operand registers (the next step's while this one computes), S = Q_prev K^T
 // by MFMA, and s <- gamma s + sum_g exp2(scale x_g - M_g) / L_g.
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
+__device__ void flush_segment_bf16(const FlushArgs& a, int lb, int h, int l, int b, int P) {
   using Cfg = MfmaCfg<D>;
   constexpr int KK = Cfg::KK, ROWB = Cfg::ROWB, STEP = Cfg::STEP;
   static_assert(G <= 8, "pending heads live in lane groups 0 and 1");
-  const int lb = blockIdx.x / a.HK;
-  const int h = blockIdx.x - lb * a.HK;
-  const int l = lb / a.B;
-  const int b = lb - l * a.B;
-  const int P = a.pend_len[lb];
-  if (P <= 0) return;
   const int n = a.len[lb];
   const int cp = a.cap[b];
   const long long sbase = a.seq_base[b];
@@ -1023,6 +1034,16 @@ __global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
   }
 }
 
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
+  const int lb = blockIdx.x / a.HK;
+  const int h = blockIdx.x - lb * a.HK;
+  const int P = a.pend_len[lb];
+  if (P <= 0) return;
+  flush_segment_bf16<D, G>(a, lb, h, lb / a.B, lb % a.B, P);
+  flush_done(a, lb);
+}
+
 // Second launch of a settling call: s <- gamma s + sum_g exp2(x_g - M_g) / L_g
 // over the rows each sequence's decode attended, from the logits that launch
 // stored and its (M, 1/L); the deferred update's arithmetic, term for term
@@ -1070,11 +1091,6 @@ __global__ __launch_bounds__(kThreads) void settle_kernel(DecodeArgs a, int nb) 
     }
     sc[j] = fmaf(a.gamma, sc[j], add);
   }
-}
-
-__global__ void flush_clear_kernel(int32_t* pend_len, int count) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < count) pend_len[i] = 0;
 }
 
 // Overrides read at every call: LETHE_DECODE_BLOCKS (blocks to aim for per
@@ -1159,9 +1175,6 @@ lethe_status launch_flush_tdg(const FlushArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((flush_bf16_kernel<D, G>), dim3((unsigned)(a.L * a.B * a.HK)), dim3(kThreads), 0, s, a);
   else
     hipLaunchKernelGGL((flush_kernel<T, D, G>), dim3((unsigned)(a.L * a.B * a.HK)), dim3(kThreads), 0, s, a);
-  if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
-  const int count = a.L * a.B;
-  hipLaunchKernelGGL(flush_clear_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, a.pend_len, count);
   return hipGetLastError() == hipSuccess ? LETHE_OK : LETHE_ERR_HIP;
 }
 

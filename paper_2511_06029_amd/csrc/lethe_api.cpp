@@ -64,6 +64,7 @@ lethe_status flush_pending(const lethe_cache* c, hipStream_t stream) {
   a.pend_scale = (const float*)(st + sl.scale_off);
   a.segstat = (const float*)(st + sl.stat_off);
   a.qprev = st + sl.q_off;
+  a.flush_cnt = (int32_t*)(st + sl.flush_cnt_off);
   return launch_flush(a, c->dtype, c->head_dim, group_size(c), stream);
 }
 

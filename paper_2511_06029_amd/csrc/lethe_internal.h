@@ -47,7 +47,7 @@ constexpr int kCntStride = 64;
 constexpr int kStepCounter = 32;
 
 struct StateLayout {
-  size_t len_off, par_off, gamma_off, scale_off, seg_cnt_off, seq_cnt_off, stat_off, q_off, total;
+  size_t len_off, par_off, gamma_off, scale_off, seg_cnt_off, seq_cnt_off, flush_cnt_off, stat_off, q_off, total;
 };
 
 inline StateLayout state_layout(int L, int B, int HK, int G, int D, size_t elem_bytes) {
@@ -59,7 +59,8 @@ inline StateLayout state_layout(int L, int B, int HK, int G, int D, size_t elem_
   s.scale_off = s.gamma_off + align_up(lb * sizeof(float), 256);
   s.seg_cnt_off = s.scale_off + align_up(lb * sizeof(float), 256);
   s.seq_cnt_off = s.seg_cnt_off + align_up((size_t)B * HK * kCntStride * sizeof(int32_t), 256);
-  s.stat_off = s.seq_cnt_off + align_up((size_t)B * kCntStride * sizeof(int32_t), 256);
+  s.flush_cnt_off = s.seq_cnt_off + align_up((size_t)B * kCntStride * sizeof(int32_t), 256);
+  s.stat_off = s.flush_cnt_off + align_up(lb * sizeof(int32_t), 256);
   s.q_off = s.stat_off + align_up(lb * HK * 2 * G * sizeof(float), 256);
   s.total = s.q_off + align_up(lb * 2 * (size_t)HK * G * D * elem_bytes, 256);
   return s;
@@ -144,6 +145,7 @@ struct FlushArgs {
   const float* pend_scale;
   const float* segstat;
   const void* qprev;
+  int32_t* flush_cnt;    // state [L][B]: flush blocks done with the pending state
 };
 
 lethe_status launch_flush(const FlushArgs& a, lethe_dtype dt, int D, int G, hipStream_t s);

@@ -251,6 +251,39 @@ def test_decode_deterministic_and_empty(monkeypatch):
     assert not np.array_equal(scores[0], host(base_score))
 
 
+@pytest.mark.parametrize("dtype,D,G,HK", [("bf16", 128, 4, 8), ("bf16", 64, 7, 2), ("f32", 64, 2, 2)])
+def test_flush_applies_once(dtype, D, G, HK):
+    """A flush applies the pending step of every (layer, sequence) and leaves
+    none: a second flush changes nothing, and the next decode step applies
+    only its own predecessor."""
+    note("flush once %s D=%d G=%d HK=%d" % (dtype, D, G, HK))
+    rng = np.random.default_rng(21 + D + G)
+    lengths = [300, 0, 1000]
+    H = Harness(3, [n + 4 for n in lengths], G * HK, HK, D, dtype)
+    for l in range(3):
+        for b, n in enumerate(lengths):
+            for h in range(HK):
+                H.fill(l, b, h, rng.standard_normal((n, D)).astype(np.float32),
+                       rng.standard_normal((n, D)).astype(np.float32), synth.score_vector(rng, n, "zipf"))
+            H.set_len(l, b, n)
+    B = len(lengths)
+    for step in range(2):
+        for l in (0, 2):  # layer 1 has no pending step
+            q = rng.standard_normal((B, G * HK, D)).astype(np.float32)
+            kn = rng.standard_normal((B, HK, D)).astype(np.float32)
+            out, ref = H.decode(l, q, kn, kn, 0.9, 0.0)
+            close(out, ref, "out step %d layer %d" % (step, l))
+        H.c.flush()
+        torch.cuda.synchronize()
+        first = host(H.c.score).copy()
+        H.c.flush()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(H.c.score), first)
+        for l in range(3):
+            H.check_scores(l)
+    assert int(H.c.dev_status[0]) == 0
+
+
 def test_decode_append_overflow_is_flagged_and_skipped():
     note("decode overflow")
     rng = np.random.default_rng(8)
