@@ -5,7 +5,8 @@ the full cached lengths of one layer: 2k, 16k, U[8k, 32k], logU[1k, 64k]) a
 two-layer cache is filled by the seeded Zipf generator and driven through
 the library with its default launch configuration (the one bench.py times):
 two decode steps with append, the second one the settling call that bench.py
-ends each interval with, then a prune round.  The oracle recomputes a
+ends each interval with, a prune round, and one decode step on the compacted
+cache.  The oracle recomputes a
 sample of segments one by one (the shortest and longest sequences and a few
 seeded picks):
 
@@ -75,7 +76,7 @@ def test_fullsize_decode_and_prune(cfg_id):
     gen = ZipfCache(cfg_id, device=DEV)
     T = gen.lengths()
     B, HQ, HK, D, G = cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.group
-    caps = [int(t) + STEPS for t in T]
+    caps = [int(t) + STEPS + 1 for t in T]
     note("fullsize config %d: B=%d HK=%d G=%d lengths %d..%d, %d layers" % (cfg_id, B, HK, G, T.min(), T.max(), LAYERS))
     c = L.LetheCache(LAYERS, caps, HQ, HK, D, dtype="bf16", device=DEV)
     for l in range(LAYERS):
@@ -176,5 +177,36 @@ def test_fullsize_decode_and_prune(cfg_id):
         np.testing.assert_array_equal(c.v[l, s0:s0 + m].view(torch.int16).cpu().numpy(), oracle.compact(vb, km))
         np.testing.assert_array_equal(c.score[l, s0:s0 + m].cpu().numpy().view(np.uint32),
                                       oracle.compact(sb, km).view(np.uint32))
+
+    # The step after the round attends the compacted cache: the oracle's
+    # segments continue from the kept rows (K, V as stored, the device's
+    # scores, which the checks above pinned bit-exactly).
+    note("fullsize config %d: decode after the prune round" % cfg_id)
+    for (l, b, h), (kb, vb, sb, km) in before.items():
+        K, V, _ = ref[l, b, h]
+        ref[l, b, h] = [K[km], V[km], sb[km].astype(np.float64)]
+    t = STEPS
+    for l in range(LAYERS):
+        q, kn, vn = gen.step(t, l, T=T + t)
+        out = torch.empty((B, HQ, D), dtype=torch.float32, device=DEV)
+        L.decode_attn_score(c, l, q, kn, vn, cfg.gamma, 0.0, out, ws)
+        torch.cuda.synchronize()
+        og, qh, kh, vh = f32(out), f32(q), f32(kn), f32(vn)
+        for b in picks:
+            for h in range(HK):
+                K, V, s = ref[l, b, h]
+                K = np.vstack([K, kh[b, h][None]])
+                V = np.vstack([V, vh[b, h][None]])
+                s = np.append(s, 0.0)
+                o, s = oracle.attend(qh[b, h * G:(h + 1) * G], K, V, s, cfg.gamma, scale)
+                ref[l, b, h] = [K, V, s]
+                close(og[b, h * G:(h + 1) * G], o, "cfg%d out after prune l%d b%d h%d" % (cfg_id, l, b, h))
+    c.flush()
+    torch.cuda.synchronize()
+    assert int(c.dev_status[0]) == 0
+    for (l, b, h), (K, V, s) in ref.items():
+        s0, _ = c.seg_rows(b, h)
+        assert int(c.len[l, b]) == K.shape[0]
+        close(f32(c.score[l, s0:s0 + K.shape[0]]), s, "cfg%d scores after prune l%d b%d h%d" % (cfg_id, l, b, h))
     del c, ws
     torch.cuda.empty_cache()
