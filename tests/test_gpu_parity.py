@@ -329,7 +329,9 @@ def _prune_harness(lengths, L_, HK, seed, kind):
 @pytest.mark.parametrize("kind", ["zipf", "ties", "special"])
 def test_select_bit_exact(kind):
     note("select %s" % kind)
-    lengths = [0, 1, 2, 64, 65, 300, 1000, 5000]
+    # Up to 8192 candidates a segment's keys stay in registers; the longer
+    # segments take the path that re-reads them.
+    lengths = [0, 1, 2, 64, 65, 300, 1000, 5000, 9000, 20000]
     H, rng = _prune_harness(lengths, 3, 2, 11, kind)
     c = H.c
     B, L_ = len(lengths), 3
@@ -351,6 +353,56 @@ def test_select_bit_exact(kind):
                     got = kh[l, start:start + n]
                     assert set(np.unique(got).tolist()) <= {0, 1}
                     np.testing.assert_array_equal(got.astype(bool), want, err_msg="l%d b%d h%d" % (l, b, h))
+
+
+def test_max_batch_decode_and_prune():
+    """The largest batch the library takes (1024 sequences): the decode's
+    blocks per segment are capped by its workspace, and the prune kernels
+    run thousands of segments.  Every sequence is checked."""
+    note("max batch")
+    rng = np.random.default_rng(31)
+    B, HK, G, D = 1024, 2, 4, 64
+    lengths = rng.integers(0, 48, B).tolist()
+    H = Harness(1, [n + 2 for n in lengths], G * HK, HK, D, "bf16")
+    K = rng.standard_normal((sum(lengths) * HK + 1, D)).astype(np.float32)
+    V = rng.standard_normal((sum(lengths) * HK + 1, D)).astype(np.float32)
+    r = 0
+    for b, n in enumerate(lengths):
+        for h in range(HK):
+            H.fill(0, b, h, K[r:r + n], V[r:r + n], synth.score_vector(rng, n, "zipf"))
+            r += n
+        H.set_len(0, b, n)
+    for step in range(2):
+        q = rng.standard_normal((B, G * HK, D)).astype(np.float32)
+        kn = rng.standard_normal((B, HK, D)).astype(np.float32)
+        out, ref = H.decode(0, q, kn, kn, 0.9, 0.0)
+        close(out, ref, "out step %d" % step)
+    H.check_scores(0)
+    c = H.c
+    bud = torch.from_numpy(np.array([[max(0, n + 2 - 5)] for n in lengths], np.int32)).to(DEV)
+    keep = torch.zeros((1, c.rows_per_layer), dtype=torch.uint8, device=DEV)
+    L.rasr_select(c, bud, 3, 1, keep)
+    torch.cuda.synchronize()
+    kh = host(keep)
+    sc = host(c.score)
+    k_before = host(c.k).copy()
+    bh = host(bud)
+    for b, n in enumerate(lengths):
+        for h in range(HK):
+            s0, _ = c.seg_rows(b, h)
+            want = oracle.rasr_select(sc[0, s0:s0 + n + 2], int(bh[b, 0]), 3, 1)
+            np.testing.assert_array_equal(kh[0, s0:s0 + n + 2].astype(bool), want, err_msg="b%d h%d" % (b, h))
+    L.kv_compact(c, keep, c.workspace(L.OP_COMPACT))
+    torch.cuda.synchronize()
+    assert int(c.dev_status[0]) == 0
+    lens = host(c.len)
+    for b, n in enumerate(lengths):
+        for h in range(HK):
+            s0, _ = c.seg_rows(b, h)
+            km = kh[0, s0:s0 + n + 2].astype(bool)
+            m = int(km.sum())
+            assert lens[0, b] == m
+            np.testing.assert_array_equal(host(c.k)[0, s0:s0 + m], k_before[0, s0:s0 + n + 2][km])
 
 
 MASKS = ["random", "first_evicted", "alternate", "last_only", "all", "none", "prefix_kept"]
