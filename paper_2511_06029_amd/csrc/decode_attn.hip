@@ -24,7 +24,10 @@
 // its query, scale and per-head (M, 1/L); the next call on the layer
 // recomputes that step's logits from the K rows it loads anyway (one more
 // MFMA chain, Q_prev K^T) and applies s <- gamma s + sum_g exp2(x_g - M_g) / L_g
-// to those rows.  launch_flush applies a pending step on its own.
+// to those rows.  launch_flush applies a pending step on its own.  A settling
+// call (the step before a prune round) also stores its raw logits per row and
+// leaves nothing pending; settle_kernel then applies its update with the same
+// arithmetic.
 //
 // Every block bumps its sequence's counter once it has read len and the
 // pending state; the block that finishes a segment publishes the new length
