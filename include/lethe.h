@@ -72,6 +72,8 @@ typedef enum { LETHE_BF16 = 0, LETHE_F32 = 1 } lethe_dtype;
 #define LETHE_DEV_INFEASIBLE 2      /* protected rows exceed the global budget        */
 #define LETHE_DEV_BAD_LAYOUT 4      /* len < 0, len > cap or segment past the layer   */
 #define LETHE_DEV_HEAD_MISMATCH 8   /* compaction kept different counts across heads  */
+#define LETHE_DEV_WAIT_TIMEOUT 16   /* a bounded wait between blocks gave up: the call's
+                                       results are unspecified (never expected)      */
 
 typedef struct {
   void* k;                  /* dtype [num_layers][rows_per_layer][head_dim]            */

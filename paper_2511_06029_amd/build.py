@@ -17,6 +17,11 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed fp32 instructions are kept out of the device code on purpose.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Per source file.  The compaction's block asks for its next queue ticket
+# (a one-lane atomic) long before it reads the reply; the atomic optimizer
+# would turn that atomic into a wave-wide one whose reply is waited for at
+# once.
+FILE_FLAGS = {"compact.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
 
 
 def sources():
@@ -33,7 +38,7 @@ def build(verbose=False):
     procs = []
     for src in sources():
         obj = os.path.join(obj_dir, os.path.basename(src) + ".o")
-        cmd = common + ["-x", "hip", "-c", src, "-o", obj]
+        cmd = common + FILE_FLAGS.get(os.path.basename(src), []) + ["-x", "hip", "-c", src, "-o", obj]
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
         objs.append(obj)
     failed = False

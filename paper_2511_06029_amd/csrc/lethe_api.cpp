@@ -95,7 +95,7 @@ size_t lethe_workspace_bytes(const lethe_cache* c, int op) {
     case LETHE_OP_SELECT:
       return 0;
     case LETHE_OP_COMPACT:
-      return align_up((size_t)c->num_layers * c->num_seqs * c->num_kv_heads * sizeof(int32_t), 256);
+      return compact_ws_bytes(c->rows_per_layer, c->num_layers, c->num_seqs, c->num_kv_heads);
   }
   return 0;
 }
@@ -374,7 +374,19 @@ lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* w
   a.HK = c->num_kv_heads;
   a.row_bytes = c->head_dim * (int32_t)elem_bytes(c->dtype);
   a.keep = keep;
-  a.counts = (int32_t*)ws;
+  const int64_t qcap = compact_queue_cap(c->rows_per_layer, a.L, a.B, a.HK);
+  if (qcap > 0x3fffffffLL) return LETHE_ERR_UNSUPPORTED;
+  char* w = (char*)ws;
+  a.counts = (int32_t*)w;
+  w += compact_counts_bytes(a.L, a.B, a.HK);
+  a.items = (CompactItem*)w;
+  w += align_up((size_t)qcap * sizeof(CompactItem), 256);
+  a.flags = (int32_t*)w;
+  a.qcap = (int32_t)qcap;
+  const StateLayout sl = state_of(c);
+  int32_t* cmp = (int32_t*)((char*)c->state + sl.cmp_off);
+  a.qlen = cmp;
+  a.ticket = cmp + kCntStride;
   a.dev_status = c->dev_status;
   return launch_compact(a, stream);
 }

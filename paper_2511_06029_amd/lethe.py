@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblethe.so
 
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
-DEV_APPEND_OVERFLOW, DEV_INFEASIBLE, DEV_BAD_LAYOUT, DEV_HEAD_MISMATCH = 1, 2, 4, 8
+DEV_APPEND_OVERFLOW, DEV_INFEASIBLE, DEV_BAD_LAYOUT, DEV_HEAD_MISMATCH, DEV_WAIT_TIMEOUT = 1, 2, 4, 8, 16
 OP_DECODE, OP_SPARSITY, OP_SELECT, OP_COMPACT, OP_DECODE_FINAL = 0, 1, 2, 3, 4
 
 SHRINK_NO_BREAKPOINT, SHRINK_NOT_TRIGGERED = -1, -2

@@ -405,13 +405,16 @@ def test_max_batch_decode_and_prune():
             np.testing.assert_array_equal(host(c.k)[0, s0:s0 + m], k_before[0, s0:s0 + n + 2][km])
 
 
-MASKS = ["random", "first_evicted", "alternate", "last_only", "all", "none", "prefix_kept"]
+MASKS = ["random", "first_evicted", "alternate", "last_only", "all", "none", "prefix_kept", "newest_evicted",
+         "front_evicted"]
 
 
 @pytest.mark.parametrize("mask", MASKS)
 def test_compact_bit_exact(mask):
     note("compact %s" % mask)
-    lengths = [1, 2, 63, 64, 65, 700, 3000]
+    # Rows move in 256-row tiles; a tile's stores wait for the earlier tiles
+    # whose rows they overwrite (up to 35 of them in the 9001-row segment).
+    lengths = [1, 2, 63, 64, 65, 700, 3000, 9001]
     H, rng = _prune_harness(lengths, 2, 2, 12, "zipf")
     c = H.c
     keep = np.zeros((2, c.rows_per_layer), np.uint8)
@@ -431,6 +434,12 @@ def test_compact_bit_exact(mask):
                 m = np.ones(n, bool)
             elif mask == "none":
                 m = np.zeros(n, bool)
+            elif mask == "newest_evicted":
+                # Steady state of the decode loop: a few evictions, all among
+                # the newest quarter of the rows.
+                m = ~((j >= 3 * n // 4) & (rng.random(n) < 0.04))
+            elif mask == "front_evicted":
+                m = j >= min(600, n // 2)
             else:
                 m = j < (n + 1) // 2
             for h in range(2):
