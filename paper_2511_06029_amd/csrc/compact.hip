@@ -20,11 +20,10 @@
 // the rows at their destinations.  So that a tile costs about one memory
 // round trip, a block asks for its next ticket as soon as it has the current
 // one, reads the flags it waits for together with the rows, and loads the
-// next entry before its stores go out.  (The counter serves one request at a
-// time, about 17 ns each: a queue of a million tiles takes 20 ms of tickets.
-// Tickets of several entries would either put consecutive tiles of a segment
-// in one block, one after the other, or make a tile wait for a later ticket,
-// which only a launch whose blocks are all resident could allow.)
+// next entry before its stores go out.  (Tickets of several entries would
+// either put consecutive tiles of a segment in one block, one after the
+// other, or make a tile wait for a later ticket, which only a launch whose
+// blocks are all resident could allow.)
 //
 // Why the order is right: a destination never exceeds its source, so the
 // stores of a tile reach only rows below the tile's end: rows of the tile
