@@ -570,10 +570,12 @@ def cpu_baseline(cache, budget_s, gamma, log):
     rng = np.random.default_rng(0)
     lens = cache.len.cpu().numpy()
     reps = 4  # steps per segment copy: the host copies are not what is timed
+    scale = 1 / math.sqrt(cache.D)
     rows = 0
     segs = 0
     t_cpu = 0.0
     l = 0
+    kept = []  # the first segments, for the multi-thread run
     while t_cpu < budget_s and l < cache.L:
         for b in range(cache.B):
             n = int(lens[l, b])
@@ -582,10 +584,12 @@ def cpu_baseline(cache, budget_s, gamma, log):
                 K = cache.k[l, s0:s0 + n].float().cpu().numpy()
                 V = cache.v[l, s0:s0 + n].float().cpu().numpy()
                 s = cache.score[l, s0:s0 + n].double().cpu().numpy()
+                if len(kept) < 64:
+                    kept.append((K, V, s.copy()))
                 for _ in range(reps):
                     q = rng.standard_normal((cache.G, cache.D)).astype(np.float32)
                     t = time.perf_counter()
-                    _, s = oracle.attend(q, K, V, s, gamma, 1 / math.sqrt(cache.D))
+                    _, s = oracle.attend(q, K, V, s, gamma, scale)
                     t_cpu += time.perf_counter() - t
                     rows += n
                 segs += 1
@@ -593,9 +597,44 @@ def cpu_baseline(cache, budget_s, gamma, log):
                 break
         l += 1
     tokens = rows / cache.HK
-    return {"value": tokens / t_cpu, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": "oracle decode attention + score update, %d steps on each of %d (layer, seq, kv-head) "
-                      "segments of the end-state cache (%d rows, %.1f s on one host thread)" % (reps, segs, rows, t_cpu)}
+    result = {"value": tokens / t_cpu, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+              "sample": "oracle decode attention + score update, %d steps on each of %d (layer, seq, kv-head) "
+                        "segments of the end-state cache (%d rows, %.1f s on one host thread)"
+                        % (reps, segs, rows, t_cpu)}
+    result["parallel"] = cpu_baseline_parallel(kept, reps, gamma, scale, cache.G, cache.D, cache.HK, log)
+    return result
+
+
+def cpu_baseline_parallel(segments, reps, gamma, scale, G, D, HK, log, min_seconds=3.0):
+    """The same oracle steps on up to 64 of those segments, one segment per task
+    on a pool of host threads (the oracle's C code runs without the GIL), for at
+    least min_seconds of wall time."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle
+
+    threads = max(1, min(16, os.cpu_count() or 1))
+    log("cpu baseline: the same oracle steps on %d segments over %d threads" % (len(segments), threads))
+    qs = [np.random.default_rng(1 + i).standard_normal((reps, G, D)).astype(np.float32) for i in range(len(segments))]
+
+    def run(i):
+        K, V, s = segments[i]
+        for r in range(reps):
+            _, s = oracle.attend(qs[i][r], K, V, s, gamma, scale)
+        return reps * K.shape[0]
+
+    rows, passes = 0, 0
+    t = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=threads) as pool:
+        while passes == 0 or time.perf_counter() - t < min_seconds:
+            rows += sum(pool.map(run, range(len(segments))))
+            passes += 1
+    dt = time.perf_counter() - t
+    return {"value": rows / HK / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": "%d passes of %d steps on each of %d segments (%d rows) over %d host threads, %.1f s wall"
+                      % (passes, reps, len(segments), rows, threads, dt)}
 
 
 if __name__ == "__main__":
