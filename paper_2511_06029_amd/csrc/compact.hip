@@ -6,39 +6,43 @@
 // rows before the first evicted row stay where they are (it is found with 32
 // independent flag loads per lane).  From the 256-row tile holding that row
 // to the end, the wavefront takes the keep mask and kept count of every tile
-// and appends the tiles, in row order, to a work queue (one append per block
-// of eight segments: a single counter serves every append); an entry carries
-// the tile's source rows, its keep mask and the destination of its first
-// kept row (the rows kept before it).
+// and groups consecutive tiles into queue entries of up to four tiles that
+// keep at most 256 rows between them (sparse tiles, as in the first round of
+// a full cache, share an entry; dense ones have one each).  It appends the
+// entries, in row order, to a work queue (one append per block of eight
+// segments); an entry carries its source rows, their keep masks, the
+// destination of its first kept row (the rows kept before it) and the flags
+// of the earlier tiles its stores overwrite.  Every tile has a flag.
 //
 // compact_move_kernel, persistent: blocks take queue entries in queue order
-// from a ticket counter.  For an entry the block lists the tile's kept rows
-// from the mask, loads them into registers (16 bytes per lane), and once
-// every load has completed marks the entry's flag.  It then waits for the
-// flags of the earlier tiles of the segment whose rows its stores overwrite
-// (at most two: the stores cover at most 256 consecutive rows), and stores
-// the rows at their destinations.  So that a tile costs about one memory
+// from a ticket counter.  For an entry the block lists the kept rows from the
+// masks, loads them into registers (16 bytes per lane), and once every load
+// has completed sets its tiles' flags.  It then waits for the flags of the
+// earlier tiles whose rows its stores overwrite (at most two: the stores
+// cover at most 256 consecutive rows, and every tile spans 256), and stores
+// the rows at their destinations.  So that an entry costs about one memory
 // round trip, a block asks for its next ticket as soon as it has the current
 // one, reads the flags it waits for together with the rows, and loads the
 // next entry before its stores go out.  (Tickets of several entries would
 // either put consecutive tiles of a segment in one block, one after the
-// other, or make a tile wait for a later ticket, which only a launch whose
+// other, or make an entry wait for a later ticket, which only a launch whose
 // blocks are all resident could allow.)
 //
 // Why the order is right: a destination never exceeds its source, so the
-// stores of a tile reach only rows below the tile's end: rows of the tile
-// itself (all loaded before the block's barrier) or of earlier tiles of the
+// stores of an entry reach only rows below the entry's end: rows of its own
+// tiles (all loaded before the block's barrier) or of earlier tiles of the
 // same segment (loaded before their flags were set).  No block reads a row
 // another block of the launch writes, so the flags order loads before stores
 // and carry no data; they need no acquire or release.  Why every wait ends: a
-// block sets its entry's flag before it waits for anything, and the entries it
-// waits for were taken from the ticket counter before its own, by blocks that
-// are running or done.  A bounded spin still turns a wait that would not end
-// into LETHE_DEV_WAIT_TIMEOUT instead of a hang.
+// block sets its tiles' flags before it waits for anything, and the entries
+// holding the tiles it waits for were taken from the ticket counter before
+// its own, by blocks that are running or done.  A bounded spin still turns a
+// wait that would not end into LETHE_DEV_WAIT_TIMEOUT instead of a hang.
 //
 // compact_len_kernel sets the new lengths and resets the queue counters for
 // the next call.
 #include "device_common.h"
+#include "compact_internal.h"
 #include "lethe_internal.h"
 
 namespace lethe {
@@ -67,11 +71,14 @@ __device__ inline CompactItem load_item(const ConstItem* p) {
   r.j0 = p->j0;
   r.end = p->end;
   r.base = p->base;
-  r.wnear = p->wnear;
-  r.wfar = p->wfar;
-  r.pad = 0;
+  r.tiles = p->tiles;
+  r.flag0 = p->flag0;
+  r.wlo = p->wlo;
+  r.whi = p->whi;
 #pragma unroll
-  for (int x = 0; x < 4; ++x) r.kept[x] = p->kept[x];
+  for (int x = 0; x < 7; ++x) r.pad[x] = 0;
+#pragma unroll
+  for (int x = 0; x < 4 * kCompactGroup; ++x) r.kept[x] = p->kept[x];
   return r;
 }
 
@@ -81,8 +88,9 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(CompactArgs 
   const int w = tid / kWave;
   const long long nseg = (long long)a.L * a.B * a.HK;
   const long long cidx = (long long)blockIdx.x * kPlanWaves + w;  // this wave's segment
-  __shared__ int s_m[kPlanWaves];
-  __shared__ int s_base;
+  __shared__ int s_m[kPlanWaves];  // moved tiles per segment
+  __shared__ int s_e[kPlanWaves];  // queue entries per segment
+  __shared__ int s_base, s_ebase;
 
   // The wave's segment: its length, first evicted row and moved tiles.
   bool valid = false;
@@ -127,19 +135,54 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(CompactArgs 
     ft = first / kTile;
     nt = first < n ? (n + kTile - 1) / kTile : ft;
   }
-  // One queue append for the block's segments.
-  if (lane == 0) s_m[w] = nt - ft;
+  // Pass 1: kept count of every moved tile and the number of entries: runs of
+  // up to kCompactGroup tiles that keep at most kTile rows between them.
+  int ne = 0;
+  {
+    int glen = 0, gcnt = 0;
+    for (int g = ft; g < nt; g += 4) {
+      uint8_t f[4][4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) f[u][x] = keep[min((g + u) * kTile + kWave * x + lane, n - 1)];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int t = g + u;
+        if (t >= nt) break;
+        int kc = 0;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) kc += __popcll(__ballot(t * kTile + kWave * x + lane < n && f[u][x] != 0));
+        if (glen > 0 && (gcnt + kc > kTile || glen == kCompactGroup)) {
+          ++ne;
+          glen = gcnt = 0;
+        }
+        ++glen;
+        gcnt += kc;
+      }
+    }
+    if (glen > 0) ++ne;
+  }
+  // One queue append for the block's segments: tiles in the low half of the
+  // counter, entries in the high half.
+  if (lane == 0) {
+    s_m[w] = nt - ft;
+    s_e[w] = ne;
+  }
   __syncthreads();
   if (tid == 0) {
-    int total = 0;
-    for (int x = 0; x < kPlanWaves; ++x) total += s_m[x];
-    int pos = 0;
-    if (total > 0) {
-      pos = atomicAdd(a.qlen, total);
+    unsigned long long add = 0;
+    for (int x = 0; x < kPlanWaves; ++x) add += ((unsigned long long)s_e[x] << 32) + (unsigned long long)s_m[x];
+    int tpos = 0, epos = 0;
+    if (add != 0) {
+      const unsigned long long old = atomicAdd(a.qctl, add);
+      tpos = (int)(old & 0xffffffffull);
+      epos = (int)(old >> 32);
       // Only segments that overlap other sequences' rows can overfill the queue.
-      if (pos > a.qcap - total) pos = -1;
+      if (tpos > a.qcap - (int)(add & 0xffffffffull)) tpos = -1;
     }
-    s_base = pos;
+    s_base = tpos;
+    s_ebase = epos;
   }
   __syncthreads();
   if (!valid) return;
@@ -154,12 +197,35 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(CompactArgs 
     }
     return;
   }
-  int pos0 = s_base;
-  for (int x = 0; x < w; ++x) pos0 += s_m[x];
+  int tpos0 = s_base, epos = s_ebase;  // this segment's first flag and entry
+  for (int x = 0; x < w; ++x) {
+    tpos0 += s_m[x];
+    epos += s_e[x];
+  }
 
-  // Tiles ft .. nt-1, four per round: kept mask, kept count, destination of
-  // the first kept row, and the earlier tiles the stores overwrite.
+  // Pass 2: the same runs, written out.  An entry's header is written when it
+  // closes, its mask words as its tiles come.
   int running = ft * kTile;  // rows kept before tile ft: all of them
+  int glen = 0, gcnt = 0, gt0 = ft, gbase = running;
+  auto close_entry = [&]() {
+    if (lane == 0) {
+      CompactItem* it = a.items + epos;
+      it->row0 = row0;
+      it->j0 = gt0 * kTile;
+      it->end = min((gt0 + glen) * kTile, n);
+      it->base = gbase;
+      it->tiles = glen;
+      it->flag0 = tpos0 + (gt0 - ft);
+      // Destinations gbase + [0, gcnt) lie in the source ranges of tiles lo ..
+      // hi; those before tile ft never move and are never overwritten.
+      const int lo = max(ft, gbase / kTile);
+      const int hi = min(gt0 - 1, (gbase + gcnt - 1) / kTile);
+      const bool wait = gcnt > 0 && lo <= hi;
+      it->wlo = wait ? tpos0 + (lo - ft) : 0;
+      it->whi = wait ? tpos0 + (hi - ft) : -1;
+    }
+    ++epos;
+  };
   for (int g = ft; g < nt; g += 4) {
     uint8_t f[4][4];
 #pragma unroll
@@ -177,29 +243,23 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(CompactArgs 
         km[x] = __ballot(t * kTile + kWave * x + lane < n && f[u][x] != 0);
         kc += __popcll(km[x]);
       }
-      if (lane == 0) {
-        const int j0 = t * kTile;
-        CompactItem it;
-        it.row0 = row0;
-        it.j0 = j0;
-        it.end = min(j0 + kTile, n);
-        it.base = running;
-        // Destinations running + [0, kc) lie in the source ranges of tiles
-        // lo .. hi; those before tile ft never move and are never overwritten.
-        const int lo = max(ft, running / kTile);
-        const int hi = min(t - 1, (running + kc - 1) / kTile);
-        const bool wait = kc > 0 && lo <= hi;
-        it.wnear = wait ? t - hi : 0;
-        it.wfar = wait ? t - lo : 0;
-        it.pad = 0;
-#pragma unroll
-        for (int x = 0; x < 4; ++x) it.kept[x] = km[x];
-        a.items[pos0 + t - ft] = it;
-        a.flags[pos0 + t - ft] = 0;
+      if (glen > 0 && (gcnt + kc > kTile || glen == kCompactGroup)) {
+        close_entry();
+        glen = gcnt = 0;
+        gt0 = t;
+        gbase = running;
       }
+      if (lane == 0) {
+#pragma unroll
+        for (int x = 0; x < 4; ++x) a.items[epos].kept[4 * glen + x] = km[x];
+        a.flags[tpos0 + (t - ft)] = 0;
+      }
+      ++glen;
+      gcnt += kc;
       running += kc;
     }
   }
+  close_entry();
   if (lane == 0) a.counts[cidx] = running;
 }
 
@@ -216,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
   __shared__ int s_t;
   __shared__ int s_src[kTile];  // the tile's kept rows in order
   // Written by the plan launch; capped as the plan capped its appends.
-  const int total = min(*a.qlen, a.qcap);
+  const int total = min((int)(*a.qctl >> 32), a.qcap);
   int spins = 0;  // thread 0's polls so far
   const ConstItem* items = (const ConstItem*)a.items;
 
@@ -234,22 +294,29 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
     char* V = reinterpret_cast<char*>(a.v) + it.row0 * RB;
     float* S = a.score + it.row0;
 
-    int cw[kTileWaves];
+    // The entry's kept rows in order: wavefront w lists mask words w and
+    // w + 8 (words past the entry's tiles count as empty).
+    constexpr int kWords = 4 * kCompactGroup;
+    int cw[kWords];
     int cnt = 0;
 #pragma unroll
-    for (int x = 0; x < kTileWaves; ++x) {
-      cw[x] = __popcll(it.kept[x]);
+    for (int x = 0; x < kWords; ++x) {
+      cw[x] = x < 4 * it.tiles ? __popcll(it.kept[x]) : 0;
       cnt += cw[x];
     }
-    if (tid < kTile) {
-      unsigned long long m = it.kept[0];  // the wave's word, without indexing by w
 #pragma unroll
-      for (int x = 1; x < kTileWaves; ++x) m = w == x ? it.kept[x] : m;
-      if ((m >> lane) & 1ull) {
-        int before = __popcll(m & ((1ull << lane) - 1ull));
+    for (int half = 0; half < 2; ++half) {
+      const int x = w + (kThreads / kWave) * half;
+      unsigned long long m = 0;  // word x, without indexing by x
+      int before = 0;
 #pragma unroll
-        for (int x = 0; x < kTileWaves; ++x) before += x < w ? cw[x] : 0;
-        s_src[before] = it.j0 + tid;
+      for (int y = 0; y < kWords; ++y) {
+        m = y == x ? it.kept[y] : m;
+        before += y < x ? cw[y] : 0;
+      }
+      if (x < 4 * it.tiles && ((m >> lane) & 1ull)) {
+        before += __popcll(m & ((1ull << lane) - 1ull));
+        s_src[before] = it.j0 + kWave * x + lane;
       }
     }
     __syncthreads();
@@ -271,20 +338,20 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
         }
       }
     }
-    // First look at the flags this tile waits for, in flight with the rows.
+    // First look at the flags this entry waits for, in flight with the rows.
     int fnear = 1, ffar = 1;
-    if (tid == 0 && it.wnear > 0) {
-      fnear = __hip_atomic_load(&a.flags[t - it.wnear], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      ffar = __hip_atomic_load(&a.flags[t - it.wfar], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0 && it.wlo <= it.whi) {
+      fnear = __hip_atomic_load(&a.flags[it.whi], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ffar = __hip_atomic_load(&a.flags[it.wlo], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __builtin_amdgcn_s_waitcnt(0);
     if (tid == 0) s_t = tnext;
     __syncthreads();  // every load of the tile has completed
+    if (tid < it.tiles) __hip_atomic_store(&a.flags[it.flag0 + tid], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (tid == 0) {
-      __hip_atomic_store(&a.flags[t], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (fnear == 0 || ffar == 0) {
-        for (int k = it.wnear; k <= it.wfar && spins <= kSpinLimit; ++k) {
-          while (__hip_atomic_load(&a.flags[t - k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+        for (int k = it.wlo; k <= it.whi && spins <= kSpinLimit; ++k) {
+          while (__hip_atomic_load(&a.flags[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
             if (++spins > kSpinLimit) {
               atomicOr(a.dev_status, LETHE_DEV_WAIT_TIMEOUT);
               break;
@@ -319,7 +386,7 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
 __global__ void compact_len_kernel(CompactArgs a) {
   const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (i == 0) {
-    *a.qlen = 0;
+    *a.qctl = 0;
     *a.ticket = 0;
   }
   if (i >= (long long)a.L * a.B) return;

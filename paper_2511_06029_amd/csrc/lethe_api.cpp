@@ -3,6 +3,7 @@
 // return without touching the device.
 #include <math.h>
 
+#include "compact_internal.h"
 #include "lethe_internal.h"
 
 using namespace lethe;
@@ -385,7 +386,7 @@ lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* w
   a.qcap = (int32_t)qcap;
   const StateLayout sl = state_of(c);
   int32_t* cmp = (int32_t*)((char*)c->state + sl.cmp_off);
-  a.qlen = cmp;
+  a.qctl = (unsigned long long*)cmp;
   a.ticket = cmp + kCntStride;
   a.dev_status = c->dev_status;
   return launch_compact(a, stream);

@@ -222,58 +222,4 @@ struct SelectArgs {
 
 lethe_status launch_select(const SelectArgs& a, hipStream_t s);
 
-// Compaction moves rows in tiles of this many source rows.
-constexpr int kCompactTile = 256;
-
-// One queue entry of the compaction: a tile of one segment whose kept rows
-// move.  The tiles of a segment are consecutive in the queue, in row order.
-struct CompactItem {
-  long long row0;  // first row of the segment (layer offset included)
-  int32_t j0;      // first source row of the tile, relative to the segment
-  int32_t end;     // one past the tile's last source row (<= len)
-  int32_t base;    // destination of the tile's first kept row (rows kept before j0)
-  // The earlier tiles whose source rows the tile's stores overwrite are the
-  // queue entries wnear .. wfar places before this one (none if wnear == 0;
-  // at most two, since the stores cover at most 256 consecutive rows).
-  int32_t wnear, wfar;
-  int32_t pad;
-  unsigned long long kept[4];  // bit i of word x: source row j0 + 64 x + i is kept
-};
-static_assert(sizeof(CompactItem) == 64, "queue entry");
-
-// Queue entries a compaction workspace holds: every segment's tiles, each
-// segment rounding up once.
-inline int64_t compact_queue_cap(int64_t rows_per_layer, int L, int B, int HK) {
-  return (int64_t)L * ((rows_per_layer + kCompactTile - 1) / kCompactTile + (int64_t)B * HK);
-}
-
-// Compaction workspace: kept counts [L][B][HK], queue entries, per-entry flags.
-inline size_t compact_counts_bytes(int L, int B, int HK) { return align_up((size_t)L * B * HK * sizeof(int32_t), 256); }
-inline size_t compact_ws_bytes(int64_t rows_per_layer, int L, int B, int HK) {
-  const size_t q = (size_t)compact_queue_cap(rows_per_layer, L, B, HK);
-  return compact_counts_bytes(L, B, HK) + align_up(q * sizeof(CompactItem), 256) + align_up(q * sizeof(int32_t), 256);
-}
-
-struct CompactArgs {
-  void* k;
-  void* v;
-  float* score;
-  int32_t* len;
-  const int64_t* seq_base;
-  const int32_t* cap;
-  int64_t rows_per_layer;
-  int32_t L, B, HK;
-  int32_t row_bytes;      // D * element size
-  const uint8_t* keep;
-  int32_t* counts;        // ws [L][B][HK]
-  CompactItem* items;     // ws [qcap]
-  int32_t* flags;         // ws [qcap]: the entry's loads are done
-  int32_t qcap;
-  int32_t* qlen;          // decode state: entries appended (reset by the last launch)
-  int32_t* ticket;        // decode state: entries taken (reset by the last launch)
-  int32_t* dev_status;
-};
-
-lethe_status launch_compact(const CompactArgs& a, hipStream_t s);
-
 }  // namespace lethe
