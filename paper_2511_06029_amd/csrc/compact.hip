@@ -57,7 +57,9 @@ constexpr int kPlanWaves = kPlanThreads / kWave;
 // Upper bound on the flag polls of one block over the whole launch (a poll is
 // a short sleep and a load from memory, about a microsecond): one to two
 // seconds, against at most the launch's own duration (milliseconds) for real
-// waits.  A block past it waits no more.
+// waits.  A block past it waits no more.  LETHE_COMPACT_SPIN_LIMIT lowers it;
+// LETHE_COMPACT_TEST_WAIT=1 makes every entry also wait for a flag nothing
+// sets, so that tests can drive the timeout path (every block still exits).
 constexpr int kSpinLimit = 1 << 20;
 // 16 bytes of a row; a vector type, so arrays of them stay in registers.
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
@@ -165,6 +167,7 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(CompactArgs 
   }
   // One queue append for the block's segments: tiles in the low half of the
   // counter, entries in the high half.
+  if (blockIdx.x == 0 && tid == 0) a.flags[a.qcap] = 0;  // the flag nothing sets
   if (lane == 0) {
     s_m[w] = nt - ft;
     s_e[w] = ne;
@@ -349,17 +352,19 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
     __syncthreads();  // every load of the tile has completed
     if (tid < it.tiles) __hip_atomic_store(&a.flags[it.flag0 + tid], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (tid == 0) {
-      if (fnear == 0 || ffar == 0) {
-        for (int k = it.wlo; k <= it.whi && spins <= kSpinLimit; ++k) {
-          while (__hip_atomic_load(&a.flags[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-            if (++spins > kSpinLimit) {
-              atomicOr(a.dev_status, LETHE_DEV_WAIT_TIMEOUT);
-              break;
-            }
-            __builtin_amdgcn_s_sleep(2);
+      auto wait_flag = [&](int k) {
+        while (spins <= a.spin_limit &&
+               __hip_atomic_load(&a.flags[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+          if (++spins > a.spin_limit) {
+            atomicOr(a.dev_status, LETHE_DEV_WAIT_TIMEOUT);
+            break;
           }
+          __builtin_amdgcn_s_sleep(2);
         }
-      }
+      };
+      if (fnear == 0 || ffar == 0)
+        for (int k = it.wlo; k <= it.whi; ++k) wait_flag(k);
+      if (a.test_wait) wait_flag(a.qcap);
     }
     const int tn = __builtin_amdgcn_readfirstlane(s_t);
     CompactItem itn = it;
@@ -401,20 +406,27 @@ __global__ void compact_len_kernel(CompactArgs a) {
   a.len[i] = mn;
 }
 
+int env_int(const char* name, int dflt) {
+  const char* e = getenv(name);
+  const int v = e ? atoi(e) : 0;
+  return v > 0 ? v : dflt;
+}
+
 int move_blocks() {
   // Persistent grid: two resident blocks per CU (the 256-byte-row kernel
-  // holds 127 VGPRs, four waves per SIMD).
-  static const int n = [] {
-    const char* e = getenv("LETHE_COMPACT_BLOCKS");
-    const int v = e ? atoi(e) : 0;
-    return v > 0 ? v : 512;
-  }();
+  // holds 119 VGPRs, four waves per SIMD).
+  static const int n = env_int("LETHE_COMPACT_BLOCKS", 512);
   return n;
 }
 
 }  // namespace
 
-lethe_status launch_compact(const CompactArgs& a, hipStream_t s) {
+lethe_status launch_compact(const CompactArgs& args, hipStream_t s) {
+  static const int spin_limit = env_int("LETHE_COMPACT_SPIN_LIMIT", kSpinLimit);
+  static const int test_wait = env_int("LETHE_COMPACT_TEST_WAIT", 0);
+  CompactArgs a = args;
+  a.spin_limit = std::min(spin_limit, kSpinLimit);
+  a.test_wait = test_wait;
   long long nb = (long long)a.L * a.B * a.HK;
   if (nb > 0x7fffffffLL) return LETHE_ERR_UNSUPPORTED;
   if (a.row_bytes != 128 && a.row_bytes != 256 && a.row_bytes != 512) return LETHE_ERR_UNSUPPORTED;

@@ -39,11 +39,13 @@ inline int64_t compact_queue_cap(int64_t rows_per_layer, int L, int B, int HK) {
   return (int64_t)L * ((rows_per_layer + kCompactTile - 1) / kCompactTile + (int64_t)B * HK);
 }
 
-// Compaction workspace: kept counts [L][B][HK], queue entries, per-tile flags.
+// Compaction workspace: kept counts [L][B][HK], queue entries, per-tile flags
+// (and one flag that is never set).
 inline size_t compact_counts_bytes(int L, int B, int HK) { return align_up((size_t)L * B * HK * sizeof(int32_t), 256); }
 inline size_t compact_ws_bytes(int64_t rows_per_layer, int L, int B, int HK) {
   const size_t q = (size_t)compact_queue_cap(rows_per_layer, L, B, HK);
-  return compact_counts_bytes(L, B, HK) + align_up(q * sizeof(CompactItem), 256) + align_up(q * sizeof(int32_t), 256);
+  return compact_counts_bytes(L, B, HK) + align_up(q * sizeof(CompactItem), 256) +
+         align_up((q + 1) * sizeof(int32_t), 256);
 }
 
 struct CompactArgs {
@@ -60,7 +62,9 @@ struct CompactArgs {
   int32_t* counts;        // ws [L][B][HK]
   CompactItem* items;     // ws [qcap]
   int32_t* flags;         // ws [qcap]: per tile, its rows are loaded
-  int32_t qcap;           // tiles (and so entries) the queue holds at most
+  int32_t qcap;           // tiles (and so entries) the queue holds at most; flags[qcap] is never set
+  int32_t spin_limit;     // flag polls a move block may spend in all
+  int32_t test_wait;      // non-zero: every entry also waits for flags[qcap] (failure-path tests)
   // Decode state, returned to zero by the last launch: tiles appended (low
   // 32 bits) and entries appended (high 32 bits); entries taken.
   unsigned long long* qctl;
