@@ -340,7 +340,14 @@ lethe_status lethe_segmented_shrink(const lethe_cache* cache, int32_t segments, 
  * len are unspecified.  keep: uint8 [num_layers][rows_per_layer].
  *  ws: lethe_workspace_bytes(cache, LETHE_OP_COMPACT) bytes.  Applies a
  *  pending decode step first (as lethe_score_flush), so the scores that move
- *  are current.
+ *  are current.  The rows move in 256-row tiles through a work queue in ws
+ *  whose counters live in the decode state, so compactions of one cache must
+ *  be ordered on one stream.  Blocks wait for one another only within a
+ *  bounded number of polls: LETHE_DEV_WAIT_TIMEOUT reports one that gave up
+ *  (not expected; the environment variables LETHE_COMPACT_TEST_WAIT=1 and
+ *  LETHE_COMPACT_SPIN_LIMIT force it, for tests), and LETHE_COMPACT_BLOCKS
+ *  overrides the 512 blocks of the moving launch.  All three are read once
+ *  per process.
  */
 lethe_status lethe_kv_compact(const lethe_cache* cache, const uint8_t* keep, void* ws,
                               size_t ws_bytes, hipStream_t stream);
