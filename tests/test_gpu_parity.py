@@ -469,6 +469,59 @@ def test_compact_bit_exact(mask):
     assert int(c.dev_status[0]) == 0
 
 
+@pytest.mark.parametrize("dtype,D", [("bf16", 64), ("f32", 128), ("f32", 64)])
+@pytest.mark.parametrize("mask", ["random", "front_evicted", "newest_evicted"])
+def test_compact_row_widths(dtype, D, mask):
+    """Compaction of 128-, 256- and 512-byte rows (its three move kernels) on
+    segments of several tiles, bit-exact against the oracle's gather."""
+    note("compact %s D=%d %s" % (dtype, D, mask))
+    lengths = [0, 1, 300, 3000, 9001]
+    rng = np.random.default_rng(21 + D)
+    H = Harness(2, [n + 3 for n in lengths], 2 * 2, 2, D, dtype)
+    c = H.c
+    for l in range(2):
+        for b, n in enumerate(lengths):
+            for h in range(2):
+                H.fill(l, b, h, rng.standard_normal((n, D)).astype(np.float32),
+                       rng.standard_normal((n, D)).astype(np.float32), synth.score_vector(rng, n, "zipf"))
+            H.set_len(l, b, n)
+    keep = np.zeros((2, c.rows_per_layer), np.uint8)
+    for l in range(2):
+        for b, n in enumerate(lengths):
+            j = np.arange(n)
+            if mask == "random":
+                m = rng.random(n) < 0.3
+            elif mask == "front_evicted":
+                m = j >= min(700, n // 2)
+            else:
+                m = ~((j >= 3 * n // 4) & (rng.random(n) < 0.05))
+            for h in range(2):
+                s0, _ = c.seg_rows(b, h)
+                keep[l, s0:s0 + n] = m
+    k_before = c.k.cpu().clone()
+    v_before = c.v.cpu().clone()
+    s_before = c.score.cpu().numpy().copy()
+    L.kv_compact(c, torch.from_numpy(keep).to(DEV), c.workspace(L.OP_COMPACT))
+    torch.cuda.synchronize()
+    assert int(c.dev_status[0]) == 0
+    bits = torch.int16 if dtype == "bf16" else torch.int32
+    kk, vv = c.k.cpu().view(bits).numpy(), c.v.cpu().view(bits).numpy()
+    kb, vb = k_before.view(bits).numpy(), v_before.view(bits).numpy()
+    ss = c.score.cpu().numpy()
+    for l in range(2):
+        for b, n in enumerate(lengths):
+            s0, _ = c.seg_rows(b, 0)
+            cnt = int(keep[l, s0:s0 + n].sum())
+            assert int(c.len[l, b]) == cnt
+            for h in range(2):
+                s0, _ = c.seg_rows(b, h)
+                m = keep[l, s0:s0 + n].astype(bool)
+                np.testing.assert_array_equal(kk[l, s0:s0 + cnt], oracle.compact(kb[l, s0:s0 + n], m))
+                np.testing.assert_array_equal(vv[l, s0:s0 + cnt], oracle.compact(vb[l, s0:s0 + n], m))
+                np.testing.assert_array_equal(ss[l, s0:s0 + cnt].view(np.uint32),
+                                              oracle.compact(s_before[l, s0:s0 + n], m).view(np.uint32))
+
+
 def test_sparsity_and_budgets():
     note("sparsity + budgets")
     lengths = [0, 1, 5, 300, 2000, 4097]
