@@ -1,25 +1,31 @@
 #!/usr/bin/env python3
 """Benchmark of the Lethe hot path on one MI355X.
 
-Workload: Llama-3-8B-shaped decoding (32 layers, 32 query / 8 KV heads,
-head_dim 128, bf16 cache), batch 8, a 2048-token prompt followed by generated
-tokens; Zipf key-bias attention with per-layer exponents s ~ U[0.8, 1.6];
-global budget 40% of the logical length split across layers by sparsity;
-a prune round every 512 decode steps with a recent window of 128.
+Default workload: the largest model-scale configuration, Llama-3-8B-shaped
+decoding (32 layers, 32 query / 8 KV heads, head_dim 128, bf16 cache) of 128
+sequences whose logical lengths are log-uniform in [1k, 64k]; a 10% global
+budget split over the layers by fixed shares of 2% to 40% (through the
+budget split's sparsity_in argument); a prune round every 128 decode steps
+with a recent window of 64.  The full caches of this batch (about 260 GB) do
+not fit one GPU with headroom, so the run starts from the steady state: every
+layer holds its budget share of each sequence.
 
-One benchmark step is one prune interval: 512 decode steps over all 32 layers
+One benchmark step is one prune interval: 128 decode steps over all 32 layers
 (append + fused attention and Eq. 5 score update: lethe_decode_attn_score),
-then one prune round over all layers.  The default run (1 warm-up step + 15
-timed steps) covers the 8192 generated tokens of the workload; inputs are
-resident in HBM before the timed region starts.
+then one prune round over all layers (lethe_layer_sparsity,
+lethe_rasr_select, lethe_kv_compact).  Inputs are resident in HBM before the
+timed region starts.  After the CPU baseline the default run frees that cache
+and runs a short leg of the Qwen-7B-shaped batch-16 workload (28 layers, 28
+query / 4 KV heads, 16k cached tokens, 30% budget, prune every 256, recent
+256; --config3-rounds intervals) and reports under "config3" what each of its
+prune rounds costs against the decode time it saves over the next interval.
 
---config 3 runs the Qwen-7B-shaped workload instead (28 layers, 28 query / 4
-KV heads, batch 16, 16k cached tokens, 2048 generated, 30% budget, prune every
-256, recent 256); --config 4 and 5 the ragged Llama-3-8B batches (64
-sequences of U[8k, 32k] cached tokens; 128 sequences of logU[1k, 64k] with
-fixed layer shares, started from the steady state since their full caches
-do not fit one GPU with headroom).  Every line also reports what each prune round costs against
-the decode time it saves over the next interval (prune_vs_saved).
+--config 2|3|4 run one of the other model-scale workloads instead (Llama-3-8B
+batch 8 with a 2k prompt and 40% budget every 512; the Qwen-7B batch-16
+workload; Llama-3-8B batch 64 of U[8k, 32k] cached tokens, 25% every 256).
+Every line reports what each prune round costs against the decode time it
+saves over the next interval (prune_vs_saved) when the run's intervals differ
+enough in size to fit the per-token decode cost.
 
 Prune rounds (--policy):
   lethe         lethe_layer_sparsity, lethe_rasr_select (a kept set per KV
@@ -33,17 +39,18 @@ Prune rounds (--policy):
                 the baselines as parameterisations of the same calls
                 (paper_2511_06029_amd/policies.py): cumulative scores and
                 uniform layer budgets; sinks plus a window filling the
-                budget; PyramidKV's static layer budgets.  Same 40% budget.
+                budget; PyramidKV's static layer budgets.
 
 With --prefill the line instead measures lethe_prefill_attn_score on the
-same model shapes: one step is the causal prefill attention with score
-seeding (Eq. 2) of a 2048-token prompt for the 8 sequences, over all 32
-layers; the roofline is the matrix-core bf16 peak.
+Llama-3-8B shapes: one step is the causal prefill attention with score
+seeding (Eq. 2) of a 2048-token prompt for 8 sequences, over all 32 layers;
+the roofline is the matrix-core bf16 peak.
 
 The JSON line reports KV tokens scanned per second (one token = one cached
 (layer, sequence, position) row, all KV heads) over the whole timed run, the
 per-step decode latency, the prune-round latency, the HBM roofline of the
-decode call and the CPU oracle's throughput on a bounded sample.
+decode call and the CPU oracle's throughput (decode step and prune round) on
+a bounded sample.
 """
 import argparse
 import ctypes
@@ -58,10 +65,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# rocprofv3 counter summary of the decode kernel on this workload (FETCH_SIZE
+# rocprofv3 counter summaries of the decode kernel per workload (FETCH_SIZE
 # and WRITE_SIZE runs); used for roofline.traffic while the kernel sources
 # still hash to the value recorded there.
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_bf16_kernel_llama8b_b8_traffic.md")
+TRAFFIC_PROFILES = {
+    2: os.path.join(ROOT, "profiles", "decode_bf16_kernel_llama8b_b8_traffic.md"),
+    5: os.path.join(ROOT, "profiles", "decode_bf16_kernel_llama8b_b128_traffic.md"),
+}
 KERNEL_SOURCES = ("paper_2511_06029_amd/csrc/decode_attn.hip", "paper_2511_06029_amd/csrc/lethe_internal.h",
                   "paper_2511_06029_amd/csrc/device_common.h")
 
@@ -69,15 +79,17 @@ KERNEL_SOURCES = ("paper_2511_06029_amd/csrc/decode_attn.hip", "paper_2511_06029
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--config", type=int, choices=(2, 3, 4, 5), default=2,
-                    help="2: Llama-3-8B shapes batch 8 (default); 3: Qwen-7B shapes batch 16, 16k cached; "
-                         "4: Llama-3-8B batch 64, lengths U[8k, 32k]; 5: Llama-3-8B batch 128, lengths "
-                         "logU[1k, 64k], fixed layer shares, from the steady state")
+    ap.add_argument("--config", type=int, choices=(2, 3, 4, 5), default=5,
+                    help="5: Llama-3-8B shapes batch 128, lengths logU[1k, 64k], fixed layer shares, from the "
+                         "steady state (default); 2: Llama-3-8B batch 8, 2k prompt; 3: Qwen-7B shapes batch 16, "
+                         "16k cached; 4: Llama-3-8B batch 64, lengths U[8k, 32k]")
     ap.add_argument("--steps", type=int, default=None,
                     help="timed prune intervals (default: the workload's generated tokens minus warm-up)")
     ap.add_argument("--warmup", type=int, default=1, help="untimed prune intervals")
-    ap.add_argument("--interval", type=int, default=None, help="decode steps per prune interval (512)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
+    ap.add_argument("--interval", type=int, default=None, help="decode steps per prune interval (the workload's)")
+    ap.add_argument("--config3-rounds", type=int, default=16,
+                    help="prune intervals of the Qwen-7B batch-16 leg after the default line's run (0: none)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline time budget of each timed part")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--policy", choices=("lethe", "lethe-shared", "shrink", "h2o", "streaming", "pyramid"),
                     default="lethe")
@@ -101,6 +113,44 @@ def main():
         run_prefill(args)
         return
 
+    import torch
+
+    def log(msg):
+        print("[bench] " + msg, file=sys.stderr, flush=True)
+
+    torch.cuda.set_device(0)
+    result, held = run_decode(args, args.config, args.steps, args.warmup, args.interval, args.policy, log,
+                              copy_probe=args.copy_probe)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(held, args.cpu_seconds, log)
+    del held
+    torch.cuda.empty_cache()
+    if args.config == 5 and args.policy == "lethe" and args.config3_rounds > 0:
+        # The prune-round target is stated at the Qwen-7B batch-16 workload: a
+        # short leg of it, after the batch-128 buffers are freed.
+        c3, held3 = run_decode(args, 3, args.config3_rounds - 1, 1, None, "lethe", log)
+        del held3
+        torch.cuda.empty_cache()
+        result["config3"] = {k: c3[k] for k in ("config", "decode_call_us", "decode_step_ms", "prune_round_us",
+                                                "select_us", "prune_vs_saved", "steps", "warmup")}
+        result["config3"]["roofline_frac"] = c3["roofline"]["frac"]
+        result["config3"]["value"] = c3["value"]
+    print(json.dumps(result), flush=True)
+
+
+WORKLOADS = {
+    2: "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128",
+    3: "qwen7b-shapes batch 16, 16k cached + generated tokens, 30% budget, prune every 256, recent 256",
+    4: "llama3-8b-shapes batch 64, cached lengths U[8k, 32k] + generated tokens, drifting heavy hitters, "
+       "25% budget, prune every 256, recent 128",
+    5: "llama3-8b-shapes batch 128, lengths logU[1k, 64k], fixed layer shares 2%-40% (10% budget), "
+       "steady-state start, prune every 128, recent 64",
+}
+
+
+def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_probe=0):
+    """Decode intervals and prune rounds of one workload.  Returns the JSON
+    fields of its line and what the CPU baseline reads (the end-state cache)."""
     import numpy as np
     import torch
 
@@ -109,22 +159,19 @@ def main():
     from workloads import CONFIGS
     from workloads.synth import ZipfCache
 
-    cfg = CONFIGS[args.config]
+    cfg = CONFIGS[cfg_id]
     dev = "cuda"
-    torch.cuda.set_device(0)
     Lyr, B, HQ, HK, D = cfg.num_layers, cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
-    interval = args.interval or cfg.prune_every
-    if args.steps is None:
-        args.steps = max(1, cfg.decode_steps // interval - args.warmup)
-    windows = args.warmup + args.steps
+    interval = interval or cfg.prune_every
+    if steps is None:
+        steps = max(1, cfg.decode_steps // interval - warmup)
+    windows = warmup + steps
     recent, sink = cfg.recent, cfg.sink
-    policy = None if args.policy == "shrink" else policies.get(args.policy, gamma=cfg.gamma, sink=sink)
+    policy = None if policy_name == "shrink" else policies.get(policy_name, gamma=cfg.gamma, sink=sink)
     gamma = policy.gamma if policy else cfg.gamma
+    log("workload %d: %s" % (cfg_id, WORKLOADS[cfg_id]))
 
-    def log(msg):
-        print("[bench] " + msg, file=sys.stderr, flush=True)
-
-    gen = ZipfCache(args.config, device=dev)
+    gen = ZipfCache(cfg_id, device=dev)
     T = gen.lengths().astype(np.int64)          # logical length of every sequence at the start
     T0 = int(T.max())
     static_s = None
@@ -142,7 +189,8 @@ def main():
     else:
         n_init = np.tile(T, (Lyr, 1))
     caps = [int(n_init[:, b].max()) + interval * windows + 1 for b in range(B)]
-    log("allocating cache: %d layers x %d seqs x %d kv heads, %d rows per layer" % (Lyr, B, HK, HK * sum(caps)))
+    log("allocating cache: %d layers x %d seqs x %d kv heads, %d rows per layer (%.1f GB)"
+        % (Lyr, B, HK, HK * sum(caps), Lyr * HK * sum(caps) * (4 * D + 4) / 1e9))
     cache = L.LetheCache(Lyr, caps, HQ, HK, D, dtype="bf16", device=dev)
     for l in range(Lyr):
         for b in range(B):
@@ -184,17 +232,17 @@ def main():
                                for b in range(B)] for w in range(windows)], np.int64)
     per_layer_dev = torch.from_numpy(per_layer_all).to(dev)
     torch.cuda.synchronize()
-    if args.copy_probe > 0:
+    if copy_probe > 0:
         # A plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings
         # calibrate the counters for the decode kernel in the same run.
-        src = torch.ones(args.copy_probe << 20, dtype=torch.uint8, device=dev)
+        src = torch.ones(copy_probe << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-        log("copy probe: 3 x %d MiB device-to-device" % args.copy_probe)
+        log("copy probe: 3 x %d MiB device-to-device" % copy_probe)
 
     lib = L.load()
     cref = ctypes.byref(cache.c_struct())
@@ -212,7 +260,7 @@ def main():
     len_snap = [torch.empty((Lyr, B), dtype=torch.int32, pin_memory=True) for _ in range(windows + 1)]
     win_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(windows)]
 
-    def run_window(w, timed):
+    def run_window(w):
         len_snap[w].copy_(cache.len, non_blocking=True)
         win_ev[w][0].record(stream)
         for i in range(interval):
@@ -224,7 +272,7 @@ def main():
                 if rc != 0:
                     raise RuntimeError("lethe_decode_attn_score: %s" % L.status_string(rc))
         win_ev[w][1].record(stream)
-        if args.policy == "shrink":
+        if policy_name == "shrink":
             L.score_flush(cache)
             win_ev[w][2].record(stream)
             L.segmented_shrink(cache, args.segments, args.tau, recent, sink, evict, None, keep)
@@ -241,14 +289,14 @@ def main():
             prune.compact()
         win_ev[w][4].record(stream)
 
-    log("warm-up: %d interval(s) of %d decode steps" % (args.warmup, interval))
-    for w in range(args.warmup):
-        run_window(w, False)
+    log("warm-up: %d interval(s) of %d decode steps" % (warmup, interval))
+    for w in range(warmup):
+        run_window(w)
     torch.cuda.synchronize()
-    log("timed: %d interval(s)" % args.steps)
+    log("timed: %d interval(s)" % steps)
     t0 = time.perf_counter()
-    for w in range(args.warmup, windows):
-        run_window(w, True)
+    for w in range(warmup, windows):
+        run_window(w)
         log("interval %d enqueued" % w)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -256,6 +304,7 @@ def main():
     status = int(cache.dev_status[0])
     if status != 0:
         raise RuntimeError("device status bits set: %d" % status)
+    log("timed intervals done")
 
     # Work accounting from the length snapshots (lengths at the start of each
     # interval; every decode step appends one row before attending).
@@ -263,29 +312,29 @@ def main():
     row_bytes = HK * (2 * D * elem + 8)               # K + V + score read/write, all KV heads
     fixed_bytes = B * HQ * D * (elem + 4) + 2 * B * HK * D * elem
     tokens = 0
-    for w in range(args.warmup, windows):
+    for w in range(warmup, windows):
         n0 = len_snap[w].numpy().astype(np.int64)
         tokens += interval * int(n0.sum()) + Lyr * B * interval * (interval + 1) // 2
     elapsed = t1 - t0
-    decode_ms = [win_ev[w][0].elapsed_time(win_ev[w][1]) for w in range(args.warmup, windows)]
-    prune_ms = [win_ev[w][1].elapsed_time(win_ev[w][4]) for w in range(args.warmup, windows)]
-    select_ms = [win_ev[w][2].elapsed_time(win_ev[w][3]) for w in range(args.warmup, windows)]
+    decode_ms = [win_ev[w][0].elapsed_time(win_ev[w][1]) for w in range(warmup, windows)]
+    prune_ms = [win_ev[w][1].elapsed_time(win_ev[w][4]) for w in range(warmup, windows)]
+    select_ms = [win_ev[w][2].elapsed_time(win_ev[w][3]) for w in range(warmup, windows)]
     # Roofline of lethe_decode_attn_score: one kernel launch per call, back to
     # back on the launch stream; the events bracket every decode call of the
     # timed intervals, so their span / calls is the average launch duration
     # (the settling calls' second, small kernel included: one step in an
     # interval).
-    n_calls = args.steps * interval * Lyr
+    n_calls = steps * interval * Lyr
     avg_call_s = float(np.sum(decode_ms)) / 1e3 / n_calls
     avg_call_bytes = (tokens * row_bytes + n_calls * fixed_bytes) / n_calls
     achieved = avg_call_bytes / avg_call_s / 1e9
-    traffic = load_traffic(avg_call_bytes) if args.config == 2 and args.policy == "lethe" else None
+    traffic = load_traffic(cfg_id, avg_call_bytes) if policy_name == "lethe" else None
 
     # Selection reads every live score once per KV head and writes a mask
     # byte per row and head (lengths at the end of each interval, before
     # compaction).
     sel_rows = 0
-    for w in range(args.warmup, windows):
+    for w in range(warmup, windows):
         sel_rows += int(len_snap[w].numpy().astype(np.int64).sum()) + Lyr * B * interval
     select_gbs = sel_rows * HK * 5 / (float(np.sum(select_ms)) / 1e3) / 1e9
 
@@ -314,45 +363,39 @@ def main():
             "per_round": ratios, "decode_ms_per_token_step": float(slope), "decode_step_fixed_ms": float(icpt),
             "prune_round_ms": [float(x) for x in all_prune],
         }
-    workload = {
-        2: "llama3-8b-shapes batch 8, 2k prompt + generated tokens, 40% budget, prune every 512, recent 128",
-        3: "qwen7b-shapes batch 16, 16k cached + generated tokens, 30% budget, prune every 256, recent 256",
-        4: "llama3-8b-shapes batch 64, cached lengths U[8k, 32k] + generated tokens, drifting heavy hitters, "
-           "25% budget, prune every 256, recent 128",
-        5: "llama3-8b-shapes batch 128, lengths logU[1k, 64k], fixed layer shares 2%-40% (10% budget), "
-           "steady-state start, prune every 128, recent 64",
-    }[args.config]
-    if args.policy == "lethe-shared":
+    workload = WORKLOADS[cfg_id]
+    if policy_name == "lethe-shared":
         workload += ", one kept set per layer and sequence"
-    elif args.policy in ("h2o", "streaming", "pyramid"):
-        workload = workload.replace("40% budget", "40%% budget, %s rule" % args.policy)
-    elif args.policy == "shrink":
+    elif policy_name in ("h2o", "streaming", "pyramid"):
+        workload += ", %s rule" % policy_name
+    elif policy_name == "shrink":
         workload = ("%s-shapes batch %d, %d cached + generated tokens, Algorithm 1 shrinking every %d "
                     "(D=%d, tau=%g, recent %d, first threshold %d)" % (
-                        "qwen7b" if args.config == 3 else "llama3-8b", B, T0, interval, args.segments, args.tau,
+                        "qwen7b" if cfg_id == 3 else "llama3-8b", B, T0, interval, args.segments, args.tau,
                         recent, T0))
     result = {
         "metric": "KV tokens scanned/s (fused decode-attn+score, prune rounds included)",
         "value": value,
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": elapsed * 1e3 / args.steps,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": elapsed * 1e3 / steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16",
         "data": "synthetic (seeded Zipf key-bias caches, random queries)",
         "config": {
             "workload": workload,
             "layers": Lyr, "q_heads": HQ, "kv_heads": HK, "head_dim": D, "batch": B, "storage": "bf16",
+            "accumulation": "fp32",
             "prompt": T0 if cfg.length_dist == "fixed" else "%s%s" % (cfg.length_dist, list(cfg.length_range)),
             "generated": interval * windows, "interval": interval, "gamma": gamma,
         },
         "decode_step_ms": float(np.mean(decode_ms)) / interval,
         "prune_round_us": float(np.mean(prune_ms)) * 1e3,
-        "policy": args.policy,
+        "policy": policy_name,
         "settled_last_step": not args.no_settle,
         "select_us": float(np.mean(select_ms)) * 1e3,
         "select_hbm_gbs": select_gbs,
@@ -368,10 +411,10 @@ def main():
         "final_lengths_mean": float(len_snap[windows].numpy().mean()),
         "prune_vs_saved": prune_vs_saved,
     }
-
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(cache, args.cpu_seconds, gamma, log)
-    print(json.dumps(result), flush=True)
+    held = {"cache": cache, "gamma": gamma, "recent": recent, "sink": sink,
+            "per_layer": per_layer_all[-1], "s_in": static_s if (policy and policy.layer_budget == "sparsity") else None}
+    del qp, kp, vp, ws, ws_c, keep, prune, evict, per_layer_dev, out
+    return result, held
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
@@ -532,13 +575,15 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def load_traffic(bytes_per_launch):
-    """HBM bytes per launch from the committed counter summary, scaled from
-    its run's algorithmic bytes per launch to this run's; None when there is
-    no summary or the kernel sources changed since it was taken."""
+def load_traffic(cfg_id, bytes_per_launch):
+    """HBM bytes per launch from the workload's committed counter summary,
+    scaled from its run's algorithmic bytes per launch to this run's; None
+    when there is no summary or the kernel sources changed since it was
+    taken."""
+    path = TRAFFIC_PROFILES.get(cfg_id)
     try:
-        text = open(TRAFFIC_PROFILE).read()
-    except OSError:
+        text = open(path).read()
+    except (OSError, TypeError):
         return None
     vals = {}
     for line in text.splitlines():
@@ -553,16 +598,52 @@ def load_traffic(bytes_per_launch):
     except (KeyError, ValueError):
         return None
     return {"bytes": measured / algorithmic * bytes_per_launch,
-            "source": "%s (ratio %.4f of algorithmic bytes)" % (os.path.relpath(TRAFFIC_PROFILE, ROOT),
-                                                                measured / algorithmic)}
+            "source": "%s (ratio %.4f of algorithmic bytes)" % (os.path.relpath(path, ROOT), measured / algorithmic)}
 
 
-def cpu_baseline(cache, budget_s, gamma, log):
+# Host threads of the parallel oracle runs: the host share one GPU has on the
+# measurement box (its nproc can show more).
+POOL_THREADS = 16
+
+
+def host_cpu():
+    """CPU model name and the number of host threads visible to this process."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        threads = len(os.sched_getaffinity(0))
+    except AttributeError:
+        threads = os.cpu_count()
+    return model, threads
+
+
+def cpu_baseline(held, budget_s, log):
+    """The oracle on the end-state cache, in the same units: its decode step
+    (attention + Eq. 5) on one host thread for about budget_s seconds, then
+    over POOL_THREADS threads; and its prune round (Hoyer sparsity of the
+    head-summed scores, the budget split, RASR selection and compaction of K,
+    V and scores) on whole sequences, likewise."""
+    model, threads = host_cpu()
+    dec = cpu_baseline_decode(held["cache"], budget_s, held["gamma"], log)
+    prune = cpu_baseline_prune(held, budget_s, log)
+    dec["cpu_model"] = model
+    dec["host_threads"] = threads
+    dec["prune_round"] = prune
+    return dec
+
+
+def cpu_baseline_decode(cache, budget_s, gamma, log):
     """The oracle's decode step on segments of the final cache, for about
     `budget_s` seconds of one host thread, in the same unit (a token is a
     (layer, sequence, position) row across all KV heads)."""
     import numpy as np
-    import torch
 
     import oracle
 
@@ -615,7 +696,7 @@ def cpu_baseline_parallel(segments, reps, gamma, scale, G, D, HK, log, min_secon
 
     import oracle
 
-    threads = max(1, min(16, os.cpu_count() or 1))
+    threads = POOL_THREADS
     log("cpu baseline: the same oracle steps on %d segments over %d threads" % (len(segments), threads))
     qs = [np.random.default_rng(1 + i).standard_normal((reps, G, D)).astype(np.float32) for i in range(len(segments))]
 
@@ -635,6 +716,97 @@ def cpu_baseline_parallel(segments, reps, gamma, scale, G, D, HK, log, min_secon
     return {"value": rows / HK / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": "%d passes of %d steps on each of %d segments (%d rows) over %d host threads, %.1f s wall"
                       % (passes, reps, len(segments), rows, threads, dt)}
+
+
+def _prune_sequence(seq, recent, sink):
+    """One sequence's prune round on the oracle: layer sparsity (or the fixed
+    layer values), the budget split, RASR selection per KV head and the
+    compaction of K, V and scores.  Returns the rows (all KV heads counted
+    once per position) it went through."""
+    import numpy as np
+
+    import oracle
+
+    layers, s_in, G_b = seq
+    L = len(layers)
+    n = np.array([lay[0].shape[1] for lay in layers], np.int32)
+    if s_in is None:
+        S = np.array([oracle.layer_sparsity(lay[0]) for lay in layers], np.float32)
+    else:
+        S = np.asarray(s_in, np.float32)
+    budget, _ = oracle.budget_split(n, S, recent, sink, G_b)
+    for l in range(L):
+        s_h, K_h, V_h = layers[l]
+        for h in range(s_h.shape[0]):
+            keep = oracle.rasr_select(s_h[h].astype(np.float32), int(budget[l]), recent, sink)
+            oracle.compact(K_h[h], keep)
+            oracle.compact(V_h[h], keep)
+            oracle.compact(s_h[h], keep)
+    return int(n.sum())
+
+
+def cpu_baseline_prune(held, budget_s, log, keep_for_parallel=16, min_seconds=3.0):
+    """The oracle's prune round on whole sequences of the end-state cache (all
+    layers and KV heads of a sequence: the budget split couples its layers),
+    one host thread for about budget_s seconds, then the first sequences over
+    POOL_THREADS threads.  The rate is in (layer, sequence, position) rows per
+    second; full_round_s scales it to every row of the cache."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    cache = held["cache"]
+    recent, sink = held["recent"], held["sink"]
+    per_layer = held["per_layer"]
+    s_in = held["s_in"]
+    lens = cache.len.cpu().numpy()
+    total_rows = int(lens.sum())
+    log("cpu baseline: oracle prune round on whole sequences (%.0f s budget)" % budget_s)
+
+    def fetch(b):
+        layers = []
+        for l in range(cache.L):
+            n = int(lens[l, b])
+            idx = [cache.seg_rows(b, h)[0] for h in range(cache.HK)]
+            s_h = np.stack([cache.score[l, i:i + n].double().cpu().numpy() for i in idx])
+            K_h = np.stack([cache.k[l, i:i + n].float().cpu().numpy() for i in idx])
+            V_h = np.stack([cache.v[l, i:i + n].float().cpu().numpy() for i in idx])
+            layers.append((s_h, K_h, V_h))
+        return (layers, s_in, int(per_layer[b]) * cache.L)
+
+    rows, seqs, t_cpu = 0, 0, 0.0
+    kept = []
+    for b in range(cache.B):
+        seq = fetch(b)
+        t = time.perf_counter()
+        rows += _prune_sequence(seq, recent, sink)
+        t_cpu += time.perf_counter() - t
+        seqs += 1
+        if len(kept) < keep_for_parallel:
+            kept.append(seq)
+        if t_cpu >= budget_s:
+            break
+    rate = rows / t_cpu
+    result = {"value": rate, "unit": "rows/s", "cores": 1, "kind": "oracle",
+              "full_round_s": total_rows / rate,
+              "sample": "oracle prune round (sparsity, budget split, RASR select, compaction of K, V and scores) "
+                        "of %d whole sequences of the end-state cache (%d (layer, seq, position) rows, %.1f s on "
+                        "one host thread); full_round_s scales it to the cache's %d rows"
+                        % (seqs, rows, t_cpu, total_rows)}
+    threads = POOL_THREADS
+    log("cpu baseline: the same prune rounds on %d sequences over %d threads" % (len(kept), threads))
+    prow, passes = 0, 0
+    t = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=threads) as pool:
+        while passes == 0 or time.perf_counter() - t < min_seconds:
+            prow += sum(pool.map(lambda sq: _prune_sequence(sq, recent, sink), kept))
+            passes += 1
+    dt = time.perf_counter() - t
+    result["parallel"] = {"value": prow / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
+                          "full_round_s": total_rows / (prow / dt),
+                          "sample": "%d passes over %d sequences (%d rows) over %d host threads, %.1f s wall"
+                                    % (passes, len(kept), prow, threads, dt)}
+    return result
 
 
 if __name__ == "__main__":

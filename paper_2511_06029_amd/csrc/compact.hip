@@ -193,17 +193,28 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(CompactArgs 
     if (lane == 0) a.counts[cidx] = n;
     return;
   }
-  if (s_base < 0) {
-    if (lane == 0) {
-      a.counts[cidx] = -1;
-      atomicOr(a.dev_status, LETHE_DEV_BAD_LAYOUT);
-    }
-    return;
-  }
   int tpos0 = s_base, epos = s_ebase;  // this segment's first flag and entry
   for (int x = 0; x < w; ++x) {
     tpos0 += s_m[x];
     epos += s_e[x];
+  }
+  if (s_base < 0) {
+    // The block's tiles did not fit the queue (only segments that overlap
+    // other sequences' rows get here).  Its entries still count in the entry
+    // half of the counter; those below the queue's end become empty entries,
+    // which the move launch skips.
+    if (lane == 0) {
+      for (int e = epos; e < epos + ne && e < a.qcap; ++e) {
+        CompactItem* it = a.items + e;
+        it->row0 = 0;
+        it->j0 = it->end = it->base = it->tiles = it->flag0 = 0;
+        it->wlo = 0;
+        it->whi = -1;
+      }
+      a.counts[cidx] = -1;
+      atomicOr(a.dev_status, LETHE_DEV_BAD_LAYOUT);
+    }
+    return;
   }
 
   // Pass 2: the same runs, written out.  An entry's header is written when it

@@ -781,8 +781,9 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   ck.segrow0 = sbase + (long long)h * cp;
   const int ps = part_stride(G, D);
 
-  // Every block of the sequence counts itself once it has read len and the
-  // pending state (a release fence orders those reads before the count).  A
+  // Every block of the sequence counts itself once all its wavefronts are
+  // done with len and the pending state: after the streaming loop, whose
+  // closing barrier every wave passes only after its last use of them.  A
   // block that finishes a segment later reads the count: all of them do so
   // after every block of its segment has counted, so the last segment to
   // finish sees the full count and publishes the new length and pending
@@ -801,8 +802,6 @@ __device__ inline void decode_body(const DecodeArgs& a) {
     pd.score = a.score + ck.segrow0;
     pd.stat = a.segstat + (long long)seg * 2 * G;
     pd.q = reinterpret_cast<const char*>(a.qprev) + par * qhalf + qgroup;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    if (tid == 0) __hip_atomic_fetch_add(seq_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return pd;
   };
   auto publish = [&](int seen) {
@@ -823,6 +822,10 @@ __device__ inline void decode_body(const DecodeArgs& a) {
       attn_chunk_mfma<D, G>(a, ck, read_pending, S.vtiles, S.cb);
     else
       attn_chunk_f32<D, G>(a, ck, read_pending, S.cb);
+    // Both routines end with a barrier that every wave reaches after its
+    // last read of len and of the pending state; their values are in
+    // registers by then, so the count cannot overtake them.
+    if (tid == 0) __hip_atomic_fetch_add(seq_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (c == 0) {
       // Keep this step's queries of the group for the next call's score update.
       const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.q) + qgroup);
@@ -1137,7 +1140,7 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   // the blocks outnumber the resident slots, and the dispatcher hands the
   // slots of early finishers to the waiting blocks.
   if (env_blocks <= 0 && nch < kMinChunksPerSeg) nch = kMinChunksPerSeg;
-  const int64_t cap_nch = decode_max_chunks(a.B, a.HK) / segs;
+  const int64_t cap_nch = a.part_cap / segs;
   if (nch > cap_nch) nch = cap_nch;
   if (nch > kMaxChunksPerSeg) nch = kMaxChunksPerSeg;
   if (nch < 1) nch = 1;

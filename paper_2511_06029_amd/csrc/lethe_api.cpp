@@ -116,21 +116,27 @@ lethe_status lethe_score_flush(const lethe_cache* c, hipStream_t stream) {
 
 namespace {
 
-lethe_status decode_call(const lethe_cache* c, int32_t layer, const void* q, const void* k_new,
-                         const void* v_new, float gamma, float softmax_scale, float* out, void* ws,
-                         size_t ws_bytes, bool settle, hipStream_t stream) {
+// Host checks of a decode call's arguments (before any HIP call).
+lethe_status check_decode(const lethe_cache* c, int32_t layer, const void* q, const void* k_new,
+                          const void* v_new, float gamma, float softmax_scale, const float* out) {
   lethe_status st = check_cache(c);
   if (st != LETHE_OK) return st;
   if (layer < 0 || layer >= c->num_layers) return LETHE_ERR_INVALID;
-  if (!q || !out || !ws) return LETHE_ERR_INVALID;
+  if (!q || !out) return LETHE_ERR_INVALID;
   if ((k_new == nullptr) != (v_new == nullptr)) return LETHE_ERR_INVALID;
   if (!(gamma > 0.0f && gamma <= 1.0f)) return LETHE_ERR_INVALID;  // also rejects NaN
   if (isnan(softmax_scale) || isinf(softmax_scale)) return LETHE_ERR_INVALID;
+  return LETHE_OK;
+}
+
+// A decode call whose arguments passed check_decode; ws holds at least one
+// chunk partial per segment (and, settling, the logits after the partials
+// of a full workspace).
+lethe_status decode_call(const lethe_cache* c, int32_t layer, const void* q, const void* k_new,
+                         const void* v_new, float gamma, float softmax_scale, float* out, void* ws,
+                         size_t ws_bytes, bool settle, hipStream_t stream) {
   const int G = group_size(c);
   const int D = c->head_dim;
-  const size_t need = settle ? decode_final_ws_bytes(c->num_seqs, c->num_kv_heads, G, D, c->rows_per_layer)
-                             : decode_ws_bytes(c->num_seqs, c->num_kv_heads, G, D);
-  if (ws_bytes < need) return LETHE_ERR_WORKSPACE;
   float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)D);
 
   const size_t eb = elem_bytes(c->dtype);
@@ -165,6 +171,8 @@ lethe_status decode_call(const lethe_cache* c, int32_t layer, const void* q, con
   a.seg_cnt = (int32_t*)(st_base + sl.seg_cnt_off);
   a.seq_cnt = (int32_t*)(st_base + sl.seq_cnt_off);
   a.part = (float*)ws;
+  const size_t part_bytes = settle ? decode_final_rows_off(c->num_seqs, c->num_kv_heads, G, D) : ws_bytes;
+  a.part_cap = (int64_t)(part_bytes / ((size_t)part_stride(G, D) * sizeof(float)));
   a.dev_status = c->dev_status;
   a.nch = 0;  // chosen by the launcher
   a.deterministic = 0;
@@ -181,6 +189,11 @@ lethe_status lethe_decode_attn_score(const lethe_cache* c, int32_t layer, const 
                                      const void* k_new, const void* v_new, float gamma,
                                      float softmax_scale, float* out, void* ws, size_t ws_bytes,
                                      hipStream_t stream) {
+  lethe_status st = check_decode(c, layer, q, k_new, v_new, gamma, softmax_scale, out);
+  if (st != LETHE_OK) return st;
+  if (!ws) return LETHE_ERR_INVALID;
+  if (ws_bytes < decode_ws_bytes(c->num_seqs, c->num_kv_heads, group_size(c), c->head_dim))
+    return LETHE_ERR_WORKSPACE;
   return decode_call(c, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, ws_bytes, false, stream);
 }
 
@@ -188,6 +201,12 @@ lethe_status lethe_decode_attn_score_final(const lethe_cache* c, int32_t layer, 
                                            const void* k_new, const void* v_new, float gamma,
                                            float softmax_scale, float* out, void* ws, size_t ws_bytes,
                                            hipStream_t stream) {
+  lethe_status st = check_decode(c, layer, q, k_new, v_new, gamma, softmax_scale, out);
+  if (st != LETHE_OK) return st;
+  if (!ws) return LETHE_ERR_INVALID;
+  if (ws_bytes < decode_final_ws_bytes(c->num_seqs, c->num_kv_heads, group_size(c), c->head_dim,
+                                       c->rows_per_layer))
+    return LETHE_ERR_WORKSPACE;
   return decode_call(c, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, ws_bytes, true, stream);
 }
 

@@ -123,6 +123,7 @@ struct DecodeArgs {
   int32_t* seg_cnt;      // [B*HK] x kCntStride
   int32_t* seq_cnt;      // [B] x kCntStride
   float* part;           // workspace
+  int64_t part_cap;      // chunk partials `part` holds (at least B * HK)
   int32_t* dev_status;
   int32_t nch;           // blocks per segment, 1 .. kMaxChunksPerSeg
   int32_t deterministic; // fixed step schedule instead of the step counter

@@ -295,10 +295,13 @@ def test_budget_equal_sparsity_splits_evenly():
     L = 7
     n = np.full(L, 1000, np.int32)
     S = np.full(L, 0.8, np.float32)
+    # Floors 16 each leave 3003 - 112 = 2891 = 7 * 413: an exact split.
     b, _ = oracle.budget_split(n, S, 16, 0, 3003)
-    assert b.tolist() == [430, 429, 429, 429, 429, 429, 428] or sorted(b.tolist()) == b.tolist()[::-1]
-    assert b.sum() == 3003 and b.max() - b.min() <= 1
-    assert list(b) == sorted(b, reverse=True)          # leftovers to lower layers
+    assert b.tolist() == [429] * 7
+    # 2893 = 7 * 413 + 2: equal remainders, so the two leftover rows go to the
+    # two lowest layers.
+    b, _ = oracle.budget_split(n, S, 16, 0, 3005)
+    assert b.tolist() == [430, 430, 429, 429, 429, 429, 429]
 
 
 def test_budget_denser_layers_get_more():
