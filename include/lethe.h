@@ -15,16 +15,18 @@
  * --------------------------------
  *  - Every pointer argument and every pointer inside lethe_cache is DEVICE
  *    memory owned by the caller, except `cache` itself, which is a host
- *    struct read during the call only.  The library allocates nothing.
+ *    struct read during the call only.  The library allocates nothing; its
+ *    only device memory of its own is that static scratch array.
  *  - Calls enqueue work on `stream` and return without synchronising the
  *    host.  The returned status covers host-checkable errors only; when it is
  *    not LETHE_OK nothing was enqueued.
  *  - Conditions found on the device are OR-ed into *cache->dev_status
  *    (LETHE_DEV_* bits below); the affected sequence or segment is left
  *    unmodified.  The caller reads the word at its own sync points.
- *  - Calls keep no global mutable state: concurrent calls on different caches
- *    and workspaces are safe.  Calls that share a cache or a workspace must be
- *    ordered on one stream.
+ *  - Calls keep no global mutable state (the one exception is the static
+ *    scratch of lethe_decode_attn_score_noalloc, shared by its calls on one
+ *    device): concurrent calls on different caches and workspaces are safe.
+ *    Calls that share a cache or a workspace must be ordered on one stream.
  *  - Each cache carries a decode state (lethe_cache::state) of
  *    lethe_state_bytes(cache) bytes that the caller allocates and zero-fills
  *    once, before the first call; the calls keep it consistent afterwards.  It
@@ -186,6 +188,34 @@ lethe_status lethe_decode_attn_score_final(const lethe_cache* cache, int32_t lay
                                            const void* k_new, const void* v_new, float gamma,
                                            float softmax_scale, float* out, void* ws, size_t ws_bytes,
                                            hipStream_t stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the decode
+ * step of lethe_decode_attn_score, items 1-3 with the same arguments, layouts,
+ * deferred score update and errors, but without a workspace argument.  The
+ * chunk partials go to a static device array of the library, 32 MiB on every
+ * device the library runs on, held until the process ends; nothing is
+ * allocated, by the library or through any other library.  The caller still
+ * owns the cache, its decode state, q, k_new, v_new and out.
+ *
+ * Every call on one device shares that device's array and leaves its
+ * partials there; each call writes every partial it reads, so no call sees an
+ * earlier call's contents.  Calls that overlap on one device (on different
+ * streams, or from different host threads without ordering) race on the
+ * array: order them on one stream.  The first call on a device looks up the
+ * array's address there (one HIP runtime query).
+ *
+ * Limit: one partial of 4 * (G * (head_dim + 2)) bytes, rounded up to 128,
+ * per (sequence, KV head) must fit the 32 MiB, i.e. num_seqs * num_kv_heads
+ * * that size <= 33554432 (all caches of up to 1024 sequences with 8 KV
+ * heads and G <= 4, or 4 KV heads and G <= 8, qualify).  Larger caches get
+ * LETHE_ERR_UNSUPPORTED before anything is enqueued.  Within the limit the
+ * call may split segments into fewer chunks than lethe_decode_attn_score.
+ */
+lethe_status lethe_decode_attn_score_noalloc(const lethe_cache* cache, int32_t layer, const void* q,
+                                             const void* k_new, const void* v_new, float gamma,
+                                             float softmax_scale, float* out, hipStream_t stream);
 
 /*
  * Causal prefill attention that seeds the importance scores, for one layer.

@@ -40,6 +40,8 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <atomic>
+
 #include "device_common.h"
 #include "lethe_internal.h"
 
@@ -1200,6 +1202,28 @@ lethe_status launch_flush_td(const FlushArgs& a, int G, hipStream_t s) {
 }
 
 }  // namespace
+
+// Chunk partials of lethe_decode_attn_score_noalloc.  Every call on a device
+// shares that device's copy; a call writes every partial it reads, so nothing
+// needs clearing between calls.  Host code uses only the address
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) char scratch[kDecodeScratchBytes];
+
+lethe_status decode_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<void*> addr[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return LETHE_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return LETHE_ERR_UNSUPPORTED;
+  void* p = addr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    // Concurrent first calls on one device store the same address.
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return LETHE_ERR_HIP;
+    addr[dev].store(p, std::memory_order_release);
+  }
+  *ptr = p;
+  return LETHE_OK;
+}
 
 lethe_status launch_decode(const DecodeArgs& a, lethe_dtype dt, int D, int G, hipStream_t s) {
   if (dt == LETHE_BF16) {

@@ -210,6 +210,21 @@ lethe_status lethe_decode_attn_score_final(const lethe_cache* c, int32_t layer, 
   return decode_call(c, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, ws_bytes, true, stream);
 }
 
+lethe_status lethe_decode_attn_score_noalloc(const lethe_cache* c, int32_t layer, const void* q,
+                                             const void* k_new, const void* v_new, float gamma,
+                                             float softmax_scale, float* out, hipStream_t stream) {
+  lethe_status st = check_decode(c, layer, q, k_new, v_new, gamma, softmax_scale, out);
+  if (st != LETHE_OK) return st;
+  // One chunk partial per segment must fit the static scratch.
+  const size_t per_chunk = (size_t)part_stride(group_size(c), c->head_dim) * sizeof(float);
+  if ((size_t)c->num_seqs * (size_t)c->num_kv_heads * per_chunk > kDecodeScratchBytes) return LETHE_ERR_UNSUPPORTED;
+  void* scratch_ptr = nullptr;
+  st = decode_scratch(&scratch_ptr);
+  if (st != LETHE_OK) return st;
+  return decode_call(c, layer, q, k_new, v_new, gamma, softmax_scale, out, scratch_ptr, kDecodeScratchBytes, false,
+                     stream);
+}
+
 lethe_status lethe_layer_sparsity(const lethe_cache* c, const int64_t* global_budget,
                                   int32_t recent, int32_t sink, const float* sparsity_in,
                                   float* sparsity_out, int32_t* budget_out, void* ws,

@@ -155,6 +155,12 @@ lethe_status launch_flush(const FlushArgs& a, lethe_dtype dt, int D, int G, hipS
 
 lethe_status launch_decode(const DecodeArgs& a, lethe_dtype dt, int D, int G, hipStream_t s);
 
+// Device scratch of lethe_decode_attn_score_noalloc: a static array of this
+// many bytes per device, holding the chunk partials of one call.
+constexpr size_t kDecodeScratchBytes = (size_t)32 << 20;
+// This device's address of that array (looked up once per device).
+lethe_status decode_scratch(void** ptr);
+
 struct SparsityArgs {
   const float* score;     // all layers
   const int32_t* len;     // [L][B]

@@ -19,6 +19,7 @@ OP_DECODE, OP_SPARSITY, OP_SELECT, OP_COMPACT, OP_DECODE_FINAL = 0, 1, 2, 3, 4
 SHRINK_NO_BREAKPOINT, SHRINK_NOT_TRIGGERED = -1, -2
 
 EXPORTED = ("lethe_workspace_bytes", "lethe_state_bytes", "lethe_decode_attn_score", "lethe_decode_attn_score_final",
+            "lethe_decode_attn_score_noalloc",
             "lethe_layer_sparsity", "lethe_rasr_select", "lethe_rasr_select_shared",
             "lethe_segmented_shrink", "lethe_kv_compact", "lethe_score_flush",
             "lethe_prefill_attn_score", "lethe_prefill_workspace_bytes", "lethe_status_string")
@@ -65,6 +66,8 @@ def load():
         lib.lethe_decode_attn_score.restype = ctypes.c_int
         lib.lethe_decode_attn_score_final.argtypes = lib.lethe_decode_attn_score.argtypes
         lib.lethe_decode_attn_score_final.restype = ctypes.c_int
+        lib.lethe_decode_attn_score_noalloc.argtypes = [pc, i32, vp, vp, vp, ctypes.c_float, ctypes.c_float, vp, vp]
+        lib.lethe_decode_attn_score_noalloc.restype = ctypes.c_int
         lib.lethe_layer_sparsity.argtypes = [pc, vp, i32, i32, vp, vp, vp, vp, sz, vp]
         lib.lethe_layer_sparsity.restype = ctypes.c_int
         lib.lethe_rasr_select.argtypes = [pc, vp, i32, i32, vp, vp, sz, vp]
@@ -139,6 +142,15 @@ def decode_attn_score_final(cache, layer, q, k_new, v_new, gamma, softmax_scale,
                                               _p(v_new), float(gamma), float(softmax_scale), _p(out), _p(ws),
                                               ws.numel() * ws.element_size(), _stream(stream))
     _check("lethe_decode_attn_score_final", st)
+
+
+def decode_attn_score_noalloc(cache, layer, q, k_new, v_new, gamma, softmax_scale, out, stream=None):
+    """lethe_decode_attn_score_noalloc: the decode step without a workspace
+    (the chunk partials use the library's static device scratch)."""
+    st = load().lethe_decode_attn_score_noalloc(ctypes.byref(cache.c_struct()), int(layer), _p(q), _p(k_new),
+                                                _p(v_new), float(gamma), float(softmax_scale), _p(out),
+                                                _stream(stream))
+    _check("lethe_decode_attn_score_noalloc", st)
 
 
 def layer_sparsity(cache, global_budget, recent, sink, sparsity_in, sparsity_out, budget_out,
