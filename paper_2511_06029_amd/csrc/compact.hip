@@ -415,6 +415,7 @@ __global__ void compact_len_kernel(CompactArgs a) {
   if (mn < 0) return;  // bad layout, already flagged
   if (mn != mx) atomicOr(a.dev_status, LETHE_DEV_HEAD_MISMATCH);
   a.len[i] = mn;
+  a.hint[i] = mn;
 }
 
 int env_int(const char* name, int dflt) {

@@ -69,6 +69,7 @@ struct CompactArgs {
   // 32 bits) and entries appended (high 32 bits); entries taken.
   unsigned long long* qctl;
   int32_t* ticket;
+  int32_t* hint;          // decode state [L][B]: tiling lengths, set to the new len
   int32_t* dev_status;
 };
 

@@ -182,10 +182,9 @@ __device__ void finish_single(const DecodeArgs& a, const Chunk& ck, const Combin
 // Last block of a segment: out and (M, 1/L) per head from the nne partials,
 // merged in batches of up to 16 chunks with online rescaling.
 template <int D, int G>
-__device__ void combine_segment(const DecodeArgs& a, const Chunk& ck, int nne) {
+__device__ void combine_segment(const DecodeArgs& a, const Chunk& ck, const float* part, int nne) {
   constexpr int NB = 16;
   const int ps = part_stride(G, D);
-  const float* part = a.part + (long long)ck.seg * a.nch * ps;
   float* stat = a.segstat + (long long)ck.seg * 2 * G;
   float* outb = a.out + ((long long)ck.b * a.HK * G + (long long)ck.h * G) * D;
   for (int i = threadIdx.x; i < G * D / 2; i += kThreads) {
@@ -731,23 +730,156 @@ struct AttnLds<float, D> {
   CombineLds cb;
 };
 
+// ---------------------------------------------------------------------------
+// Tiling: which chunk of which segment a block works on
+// ---------------------------------------------------------------------------
+// The launch splits every segment into chunks of about the same number of
+// 32-row steps, so that sequences of very different lengths end together.
+// The split follows the layer's tiling hints (lengths in the decode state,
+// written by flush and compaction only, so every block of a launch reads the
+// same values): with S the hinted steps of all segments and nbt the blocks
+// the launch aims for, a segment of w hinted steps gets
+// nch = clamp(ceil(w / ceil(S / nbt)), 1, kMaxChunksPerSeg) chunks, one
+// block each.  The blocks of sequence b are consecutive, KV head by KV head:
+// block P_b + h nch_b + c is chunk c of segment (b, h).  When every hint is 0
+// each segment gets nch_flat chunks.  A hint only shapes the split: every
+// chunk count covers the segment's actual rows.  Blocks past the last chunk
+// have nothing to do.
+struct SeqWords {
+  int n, cp;           // len and cap
+  long long sbase;     // seq_base
+  int pend_len, pend_par;
+  float pend_gamma, pend_scale;
+};
+
+struct BlockPlan {
+  int b = 0, nch = 1, first = 0;  // sequence, its chunks per segment, its first block
+  bool valid = false;             // the block has a chunk
+};
+
+// Inclusive prefix sum over the 64 lanes of a wavefront (DPP row shifts,
+// then the row broadcasts of lanes 15 and 31).
+__device__ inline int wave_incl_scan_i32(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
+}
+
+// Hinted steps are capped so that their sum over 1024 sequences stays an int.
+constexpr int kMaxHintSteps = 1 << 20;
+
+// The plan of block `blk` from R rows of 64 sequences (sequence 64 r + lane).
+// With kWords the sequences' own words come in the same round trip and the
+// chosen one's are returned in `w` (R = 4 covers up to 256 sequences).
+template <int R, bool kWords>
+__device__ inline BlockPlan plan_block(const DecodeArgs& a, int blk, SeqWords& w) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int B = a.B;
+  int hv[R];
+  int wn[R], wc[R], wpl[R], wpp[R];
+  long long wsb[R];
+  float wpg[R], wps[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int bb = min(kWave * r + lane, B - 1);  // clamped: every load is issued
+    hv[r] = a.hint[bb];
+    if constexpr (kWords) {
+      wn[r] = a.len[bb];
+      wc[r] = a.cap[bb];
+      wsb[r] = a.seq_base[bb];
+      wpl[r] = a.pend_len[bb];
+      wpp[r] = a.pend_par[bb];
+      wpg[r] = a.pend_gamma[bb];
+      wps[r] = a.pend_scale[bb];
+    }
+  }
+  int stp[R];
+  int sum = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const bool in = kWave * r + lane < B;
+    stp[r] = (in && hv[r] > 0) ? min((hv[r] + 31) >> 5, kMaxHintSteps) : 0;
+    sum += stp[r];
+  }
+  const long long total = (long long)__builtin_amdgcn_readlane(wave_incl_scan_i32(sum), kWave - 1) * a.HK;
+  int spb = 0;  // steps per chunk; 0: flat split
+  if (total > 0) spb = (int)min((total + a.nbt - 1) / a.nbt, (long long)kMaxHintSteps);
+  BlockPlan p;
+  int carry = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const bool in = kWave * r + lane < B;
+    const int nch = spb > 0 ? min(max((stp[r] + spb - 1) / spb, 1), kMaxChunksPerSeg) : a.nch_flat;
+    const int cnt = in ? a.HK * nch : 0;
+    const int incl = wave_incl_scan_i32(cnt);
+    const int ex = carry + incl - cnt;
+    const unsigned long long hit = __ballot(cnt > 0 && blk >= ex && blk < ex + cnt);
+    if (hit) {
+      const int src = (int)__builtin_ctzll(hit);
+      p.valid = true;
+      p.b = kWave * r + src;
+      p.nch = __builtin_amdgcn_readlane(nch, src);
+      p.first = __builtin_amdgcn_readlane(ex, src);
+      if constexpr (kWords) {
+        w.n = __builtin_amdgcn_readlane(wn[r], src);
+        w.cp = __builtin_amdgcn_readlane(wc[r], src);
+        const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)wsb[r], src);
+        const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((unsigned long long)wsb[r] >> 32), src);
+        w.sbase = (long long)(((unsigned long long)hi << 32) | lo);
+        w.pend_len = __builtin_amdgcn_readlane(wpl[r], src);
+        w.pend_par = __builtin_amdgcn_readlane(wpp[r], src);
+        w.pend_gamma = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wpg[r]), src));
+        w.pend_scale = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wps[r]), src));
+      }
+    }
+    carry += __builtin_amdgcn_readlane(incl, kWave - 1);
+  }
+  return p;
+}
+
 template <typename T, int D, int G>
 __device__ inline void decode_body(const DecodeArgs& a) {
   __shared__ __attribute__((aligned(16))) AttnLds<T, D> S;
   __shared__ int s_last;
   const int tid = threadIdx.x;
-  // Block c of segment seg: the nch blocks of a segment are spread over the
-  // grid (and over the dispatch order).
-  const int segs = a.B * a.HK;
-  const int seg = (int)(blockIdx.x % segs);
-  const int c = (int)(blockIdx.x / segs);
-  const int b = seg / a.HK;
-  const int h = seg - b * a.HK;
+  const int blk = (int)blockIdx.x;
   const int HQ = a.HK * G;
 
-  const int n = a.len[b];
-  const int cp = a.cap[b];
-  const long long sbase = a.seq_base[b];
+  // Every wave plans alike (no barrier); with up to 256 sequences the chosen
+  // sequence's words arrive with the hints.
+  SeqWords sw;
+  BlockPlan bp;
+  if (a.B <= 4 * kWave) {
+    bp = plan_block<4, true>(a, blk, sw);
+  } else {
+    bp = plan_block<kMaxSeqs / kWave, false>(a, blk, sw);
+    if (bp.valid) {
+      const int bb = bp.b;
+      sw.n = a.len[bb];
+      sw.cp = a.cap[bb];
+      sw.sbase = a.seq_base[bb];
+      sw.pend_len = a.pend_len[bb];
+      sw.pend_par = a.pend_par[bb];
+      sw.pend_gamma = a.pend_gamma[bb];
+      sw.pend_scale = a.pend_scale[bb];
+    }
+  }
+  if (!bp.valid) return;
+  const int b = bp.b;
+  const int nch = bp.nch;
+  const int o = blk - bp.first;
+  const int h = o / nch;
+  const int c = o - h * nch;
+  const int seg = b * a.HK + h;
+  const int seg_first = bp.first + h * nch;  // block (and partial) of chunk 0
+
+  const int n = sw.n;
+  const int cp = sw.cp;
+  const long long sbase = sw.sbase;
   const bool app = a.k_new != nullptr;
   const bool bad = n < 0 || cp < 0 || n > cp || sbase < 0 || sbase + (long long)a.HK * cp > a.rows_per_layer;
   const bool ovf = !bad && app && n >= cp;
@@ -776,36 +908,32 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   ck.c = c;
   ck.next = &a.seg_cnt[(long long)seg * kCntStride + kStepCounter];
   ck.first = c * kNumWaves;  // wave w starts at step c * waves + w
-  ck.stride = a.deterministic ? a.nch * kNumWaves : 0;
-  ck.dyn_base = a.nch * kNumWaves;
+  ck.stride = a.deterministic ? nch * kNumWaves : 0;
+  ck.dyn_base = nch * kNumWaves;
   ck.app = app;
   ck.ncache = n;
   ck.segrow0 = sbase + (long long)h * cp;
   const int ps = part_stride(G, D);
 
-  // Every block of the sequence counts itself once all its wavefronts are
-  // done with len and the pending state: after the streaming loop, whose
-  // closing barrier every wave passes only after its last use of them.  A
-  // block that finishes a segment later reads the count: all of them do so
-  // after every block of its segment has counted, so the last segment to
-  // finish sees the full count and publishes the new length and pending
-  // step; earlier finishers that also see it publish the same values.  The
-  // attention routines call read_pending after their first loads are out.
+  // The pending score step of this sequence (from the words read with the
+  // plan).  Every block of the sequence counts itself once all its
+  // wavefronts are done with len and the pending state: after the streaming
+  // loop, whose closing barrier every wave passes only after its last use of
+  // them.  A block that finishes a segment later reads the count: all of
+  // them do so after every block of its segment has counted, so the last
+  // segment to finish sees the full count and publishes the new length and
+  // pending step; earlier finishers that also see it publish the same values.
   int32_t* seq_ctr = &a.seq_cnt[(long long)b * kCntStride];
-  const int seq_full = a.HK * a.nch;
-  int par = 0;
-  auto read_pending = [&]() {
-    Pending<G> pd;
-    par = a.pend_par[b] & 1;
-    const int pend_rows = a.pend_len[b];
-    pd.rows = pend_rows > 0 ? min(pend_rows, n) : 0;
-    pd.gamma = a.pend_gamma[b];
-    pd.scale = a.pend_scale[b];
-    pd.score = a.score + ck.segrow0;
-    pd.stat = a.segstat + (long long)seg * 2 * G;
-    pd.q = reinterpret_cast<const char*>(a.qprev) + par * qhalf + qgroup;
-    return pd;
-  };
+  const int seq_full = a.HK * nch;
+  const int par = sw.pend_par & 1;
+  Pending<G> pd0;
+  pd0.rows = sw.pend_len > 0 ? min(sw.pend_len, n) : 0;
+  pd0.gamma = sw.pend_gamma;
+  pd0.scale = sw.pend_scale;
+  pd0.score = a.score + ck.segrow0;
+  pd0.stat = a.segstat + (long long)seg * 2 * G;
+  pd0.q = reinterpret_cast<const char*>(a.qprev) + par * qhalf + qgroup;
+  auto read_pending = [&]() { return pd0; };
   auto publish = [&](int seen) {
     if (seen != seq_full) return;
     if (app) a.len[b] = n_att;
@@ -825,8 +953,7 @@ __device__ inline void decode_body(const DecodeArgs& a) {
     else
       attn_chunk_f32<D, G>(a, ck, read_pending, S.cb);
     // Both routines end with a barrier that every wave reaches after its
-    // last read of len and of the pending state; their values are in
-    // registers by then, so the count cannot overtake them.
+    // last use of len and of the pending state.
     if (tid == 0) __hip_atomic_fetch_add(seq_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (c == 0) {
       // Keep this step's queries of the group for the next call's score update.
@@ -834,7 +961,7 @@ __device__ inline void decode_body(const DecodeArgs& a) {
       uint4* dst = reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.qprev) + (par ^ 1) * qhalf + qgroup);
       for (int i = tid; i < (int)(G * D * sizeof(T) / 16); i += kThreads) dst[i] = src[i];
     }
-    if (a.nch == 1) {
+    if (nch == 1) {
       int seen = 0;
       if (tid == 0) seen = __hip_atomic_load(seq_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       finish_single<D, G>(a, ck, S.cb);
@@ -844,14 +971,14 @@ __device__ inline void decode_body(const DecodeArgs& a) {
       }
       return;
     }
-    write_partial<D, G>(S.cb, a.part + ((long long)seg * a.nch + c) * ps);
+    write_partial<D, G>(S.cb, a.part + (long long)blk * ps);
   }
 
   // Completion count of the segment: every block, with or without steps.
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (tid == 0)
-    s_last = __hip_atomic_fetch_add(&a.seg_cnt[(long long)seg * kCntStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.nch - 1;
+    s_last = __hip_atomic_fetch_add(&a.seg_cnt[(long long)seg * kCntStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nch - 1;
   __syncthreads();
   if (!s_last) return;
   int seen = 0;
@@ -860,7 +987,7 @@ __device__ inline void decode_body(const DecodeArgs& a) {
     __hip_atomic_store(ck.next, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     seen = __hip_atomic_load(seq_ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  combine_segment<D, G>(a, ck, a.nch);
+  combine_segment<D, G>(a, ck, a.part + (long long)seg_first * ps, nch);
   if (tid == 0) publish(seen);
 }
 
@@ -953,6 +1080,7 @@ template <typename T, int D, int G>
 __global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
   const int lb = blockIdx.x / a.HK;
   const int h = blockIdx.x - lb * a.HK;
+  if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
   const int P = a.pend_len[lb];
   if (P <= 0) return;
   flush_segment_valu<T, D, G>(a, lb, h, lb / a.B, lb % a.B, P);
@@ -1046,6 +1174,7 @@ template <int D, int G>
 __global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
   const int lb = blockIdx.x / a.HK;
   const int h = blockIdx.x - lb * a.HK;
+  if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
   const int P = a.pend_len[lb];
   if (P <= 0) return;
   flush_segment_bf16<D, G>(a, lb, h, lb / a.B, lb % a.B, P);
@@ -1101,54 +1230,58 @@ __global__ __launch_bounds__(kThreads) void settle_kernel(DecodeArgs a, int nb) 
   }
 }
 
-// Overrides read at every call: LETHE_DECODE_BLOCKS (blocks to aim for per
-// launch; default two per CU and at least four per segment) and
-// LETHE_DECODE_DETERMINISTIC (non-zero: fixed step schedule, so repeated
-// calls give bit-identical results).
+// Overrides read at every call: LETHE_DECODE_BLOCKS (chunks the tiling aims
+// for) and LETHE_DECODE_DETERMINISTIC (non-zero: every wavefront's steps are
+// fixed, so repeated calls are bit-identical; by default a segment's
+// wavefronts take their steps after the first from a counter, so a block the
+// memory system serves faster takes more of them, and repeated calls differ
+// in the last bits of out and the scores).
 constexpr int64_t kMinChunksPerSeg = 4;
 int env_int(const char* name) {
   const char* v = getenv(name);
   return v ? atoi(v) : 0;
 }
 
+// Chunks a launch aims for by default: one per 2048 rows of the layer's
+// capacity (the only size the host knows), between 512 and 2048.  Measured on
+// the model-scale workloads: the Llama-8B batch-8 and Qwen-7B batch-16 caches
+// (about 1M rows per layer, 0.3M live) do best with 512-1024 chunks, the
+// Llama-8B batch-128 cache (9M rows, 1.8M live) with 2048.
+constexpr int64_t kRowsPerTargetChunk = 2048;
+constexpr int64_t kMinTarget = 512, kMaxTarget = 2048;
+
 template <typename T, int D, int G>
 lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   DecodeArgs a = a_in;
-  // Resident blocks per device for this instantiation; the value depends only
-  // on the device, so concurrent first calls store the same number.
-  static int resident[64];
   const int env_blocks = env_int("LETHE_DECODE_BLOCKS");
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return LETHE_ERR_HIP;
-  int blocks = (dev >= 0 && dev < 64) ? __atomic_load_n(&resident[dev], __ATOMIC_RELAXED) : 0;
-  if (blocks <= 0) {
-    int cus = 0, per_cu = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return LETHE_ERR_HIP;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<T, D, G>(), kThreads, 0) != hipSuccess)
-      return LETHE_ERR_HIP;
-    blocks = cus * (per_cu < 1 ? 1 : per_cu);
-    if (dev >= 0 && dev < 64) __atomic_store_n(&resident[dev], blocks, __ATOMIC_RELAXED);
-  }
-  int target = env_blocks;
+  int64_t target = env_blocks;
   if (target <= 0) {
-    int cus = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return LETHE_ERR_HIP;
-    target = blocks < 2 * cus ? blocks : 2 * cus;
+    target = a.rows_per_layer / kRowsPerTargetChunk;
+    if (target < kMinTarget) target = kMinTarget;
+    if (target > kMaxTarget) target = kMaxTarget;
   }
   a.deterministic = env_int("LETHE_DECODE_DETERMINISTIC") != 0;
   const int64_t segs = (int64_t)a.B * a.HK;
-  int64_t nch = target / segs;
-  // At least four blocks per segment: with many segments of ragged lengths
-  // the blocks outnumber the resident slots, and the dispatcher hands the
-  // slots of early finishers to the waiting blocks.
-  if (env_blocks <= 0 && nch < kMinChunksPerSeg) nch = kMinChunksPerSeg;
-  const int64_t cap_nch = a.part_cap / segs;
-  if (nch > cap_nch) nch = cap_nch;
-  if (nch > kMaxChunksPerSeg) nch = kMaxChunksPerSeg;
-  if (nch < 1) nch = 1;
-  a.nch = (int32_t)nch;
+  // Flat split (no hints yet): at least four chunks per segment, so that with
+  // many segments of ragged lengths the dispatcher hands the slots of early
+  // finishers to waiting blocks.
+  int64_t nflat = target / segs;
+  if (env_blocks <= 0 && nflat < kMinChunksPerSeg) nflat = kMinChunksPerSeg;
+  if (nflat > a.part_cap / segs) nflat = a.part_cap / segs;
+  if (nflat > kMaxChunksPerSeg) nflat = kMaxChunksPerSeg;
+  if (nflat < 1) nflat = 1;
+  // Hinted split: about `target` chunks in all, plus at most one more per
+  // segment from rounding up; one partial per block in the workspace.
+  int64_t nbt = target;
+  if (nbt > a.part_cap - segs) nbt = a.part_cap - segs;
+  if (nbt > kMaxDecodeTarget) nbt = kMaxDecodeTarget;
+  if (nbt < 1) nbt = 1;
+  a.nbt = (int32_t)nbt;
+  a.nch_flat = (int32_t)nflat;
+  int64_t grid = nbt + segs;
+  if (grid < segs * nflat) grid = segs * nflat;
   const auto kernel = decode_kernel<T, D, G>();
-  hipLaunchKernelGGL(kernel, dim3((unsigned)(segs * nch)), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kThreads), 0, s, a);
   if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
   if (a.logit) {
     // About four rows per thread at the average segment capacity.

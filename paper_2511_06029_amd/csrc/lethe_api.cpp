@@ -66,6 +66,7 @@ lethe_status flush_pending(const lethe_cache* c, hipStream_t stream) {
   a.segstat = (const float*)(st + sl.stat_off);
   a.qprev = st + sl.q_off;
   a.flush_cnt = (int32_t*)(st + sl.flush_cnt_off);
+  a.hint = (int32_t*)(st + sl.hint_off);
   return launch_flush(a, c->dtype, c->head_dim, group_size(c), stream);
 }
 
@@ -170,11 +171,12 @@ lethe_status decode_call(const lethe_cache* c, int32_t layer, const void* q, con
   a.qprev = st_base + sl.q_off + lb * 2 * (size_t)c->num_q_heads * D * eb;
   a.seg_cnt = (int32_t*)(st_base + sl.seg_cnt_off);
   a.seq_cnt = (int32_t*)(st_base + sl.seq_cnt_off);
+  a.hint = (const int32_t*)(st_base + sl.hint_off) + lb;
   a.part = (float*)ws;
   const size_t part_bytes = settle ? decode_final_rows_off(c->num_seqs, c->num_kv_heads, G, D) : ws_bytes;
   a.part_cap = (int64_t)(part_bytes / ((size_t)part_stride(G, D) * sizeof(float)));
   a.dev_status = c->dev_status;
-  a.nch = 0;  // chosen by the launcher
+  a.nbt = a.nch_flat = 0;  // chosen by the launcher
   a.deterministic = 0;
   a.logit = settle ? (float*)((char*)ws + decode_final_logit_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
   a.apply_rows = settle ? (int32_t*)((char*)ws + decode_final_rows_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
@@ -422,6 +424,7 @@ lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* w
   int32_t* cmp = (int32_t*)((char*)c->state + sl.cmp_off);
   a.qctl = (unsigned long long*)cmp;
   a.ticket = cmp + kCntStride;
+  a.hint = (int32_t*)((char*)c->state + sl.hint_off);
   a.dev_status = c->dev_status;
   return launch_compact(a, stream);
 }

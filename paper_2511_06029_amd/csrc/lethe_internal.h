@@ -13,11 +13,11 @@ namespace lethe {
 constexpr int kMaxSeqs = 1024;
 // Largest number of layers the budget split handles.
 constexpr int kMaxLayers = 256;
-// Most chunks one (sequence, KV head) segment is split into per decode call
-// (also the lane count of the combine, one chunk per lane).
+// Most chunks one (sequence, KV head) segment is split into per decode call.
 constexpr int kMaxChunksPerSeg = 64;
-// Most chunks per decode call over all segments (sizes the partial buffer).
-constexpr int kMaxDecodeChunks = 8192;
+// Most blocks a decode launch aims for beyond one per segment (the partial
+// buffer holds one partial per block: this many plus one per segment).
+constexpr int kMaxDecodeTarget = 4096;
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -39,6 +39,9 @@ __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a -
 //   seq_cnt    [B] x kCntStride     segments of a sequence done (0 between calls)
 //   segstat    [L][B*HK][2G]        per head: M (max scaled logit), then 1 / L
 //   qprev      [L][2][B][HQ][D]     queries (storage type), double buffered
+//   hint       [L][B]               lengths the decode tiling balances by
+//                                   (written by flush and compaction only,
+//                                   so a decode launch sees one value)
 // Counters sit kCntStride words apart so the atomics of different segments
 // meet in different cache lines and memory channels.  A segment's slot also
 // holds, kStepCounter words in, the counter its wavefronts take decode steps
@@ -48,7 +51,7 @@ constexpr int kStepCounter = 32;
 
 struct StateLayout {
   size_t len_off, par_off, gamma_off, scale_off, seg_cnt_off, seq_cnt_off, flush_cnt_off, cmp_off, stat_off, q_off,
-      total;
+      hint_off, total;
 };
 
 inline StateLayout state_layout(int L, int B, int HK, int G, int D, size_t elem_bytes) {
@@ -64,7 +67,8 @@ inline StateLayout state_layout(int L, int B, int HK, int G, int D, size_t elem_
   s.cmp_off = s.flush_cnt_off + align_up(lb * sizeof(int32_t), 256);
   s.stat_off = s.cmp_off + align_up(2 * kCntStride * sizeof(int32_t), 256);
   s.q_off = s.stat_off + align_up(lb * HK * 2 * G * sizeof(float), 256);
-  s.total = s.q_off + align_up(lb * 2 * (size_t)HK * G * D * elem_bytes, 256);
+  s.hint_off = s.q_off + align_up(lb * 2 * (size_t)HK * G * D * elem_bytes, 256);
+  s.total = s.hint_off + align_up(lb * sizeof(int32_t), 256);
   return s;
 }
 
@@ -73,12 +77,7 @@ inline StateLayout state_layout(int L, int B, int HK, int G, int D, size_t elem_
 __host__ __device__ inline int part_stride(int G, int D) { return (int)align_up((size_t)G * (D + 2), 32); }
 
 // Chunks the partial buffer of a decode workspace holds.
-inline int64_t decode_max_chunks(int B, int HK) {
-  const int64_t segs = (int64_t)B * HK;
-  int64_t c = segs * kMaxChunksPerSeg;
-  if (c > kMaxDecodeChunks) c = kMaxDecodeChunks;
-  return c < segs ? segs : c;
-}
+inline int64_t decode_max_chunks(int B, int HK) { return (int64_t)B * HK + kMaxDecodeTarget; }
 
 // Decode workspace: the chunk partials, scratch between calls.
 inline size_t decode_ws_bytes(int B, int HK, int G, int D) {
@@ -122,11 +121,13 @@ struct DecodeArgs {
   void* qprev;           // [2][B][HQ][D]
   int32_t* seg_cnt;      // [B*HK] x kCntStride
   int32_t* seq_cnt;      // [B] x kCntStride
-  float* part;           // workspace
+  const int32_t* hint;   // state [B] of this layer: tiling lengths
+  float* part;           // workspace: one partial per block
   int64_t part_cap;      // chunk partials `part` holds (at least B * HK)
   int32_t* dev_status;
-  int32_t nch;           // blocks per segment, 1 .. kMaxChunksPerSeg
-  int32_t deterministic; // fixed step schedule instead of the step counter
+  int32_t nbt;           // blocks the tiling aims for
+  int32_t nch_flat;      // chunks per segment when every hint is 0
+  int32_t deterministic; // fixed step schedule instead of the per-segment step counter
   // Settling call only (else null): the step's logits [rows_per_layer][8]
   // (raw q.k for bf16, scaled to log2 units for fp32) and the rows to
   // update per sequence (0: skipped), both in the workspace.
@@ -149,6 +150,7 @@ struct FlushArgs {
   const float* segstat;
   const void* qprev;
   int32_t* flush_cnt;    // state [L][B]: flush blocks done with the pending state
+  int32_t* hint;         // state [L][B]: tiling lengths, refreshed from len
 };
 
 lethe_status launch_flush(const FlushArgs& a, lethe_dtype dt, int D, int G, hipStream_t s);
