@@ -98,6 +98,10 @@ def parse():
     ap.add_argument("--prefill", action="store_true", help="time the prompt prefill with score seeding instead")
     ap.add_argument("--no-settle", action="store_true",
                     help="last step of an interval deferred like the others (the prune round then applies it)")
+    ap.add_argument("--compaction", choices=("fused", "eager"), default="eager",
+                    help="fused: the round plans the compaction and the next decode step of each layer carries it "
+                         "out (lethe_kv_compact_plan + lethe_decode_attn_score_compact); eager: lethe_kv_compact "
+                         "in the round")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="first copy MIB MiB device-to-device 3 times (counter calibration runs)")
     return ap.parse_args()
@@ -132,7 +136,8 @@ def main():
         del held3
         torch.cuda.empty_cache()
         result["config3"] = {k: c3[k] for k in ("config", "decode_call_us", "decode_step_ms", "prune_round_us",
-                                                "select_us", "prune_vs_saved", "steps", "warmup")}
+                                                "prune_kernels_us", "select_us", "compaction", "prune_vs_saved",
+                                                "steps", "warmup")}
         result["config3"]["roofline_frac"] = c3["roofline"]["frac"]
         result["config3"]["value"] = c3["value"]
     print(json.dumps(result), flush=True)
@@ -188,7 +193,7 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
                                    min(T[b], floor_rows), T[b])
     else:
         n_init = np.tile(T, (Lyr, 1))
-    caps = [int(n_init[:, b].max()) + interval * windows + 1 for b in range(B)]
+    caps = [int(n_init[:, b].max()) + interval * windows + 3 for b in range(B)]
     log("allocating cache: %d layers x %d seqs x %d kv heads, %d rows per layer (%.1f GB)"
         % (Lyr, B, HK, HK * sum(caps), Lyr * HK * sum(caps) * (4 * D + 4) / 1e9))
     cache = L.LetheCache(Lyr, caps, HQ, HK, D, dtype="bf16", device=dev)
@@ -220,7 +225,8 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
     # One workspace for both decode calls: the settling call's layout starts
     # with the deferred call's.
     ws = cache.workspace(L.OP_DECODE if args.no_settle else L.OP_DECODE_FINAL)
-    ws_c = cache.workspace(L.OP_COMPACT)
+    fused = args.compaction == "fused"
+    ws_c = cache.workspace(L.OP_COMPACT_PLAN if fused else L.OP_COMPACT)
     keep = torch.empty((Lyr, cache.rows_per_layer), dtype=torch.uint8, device=dev)
     prune = policies.PruneRound(cache, policy) if policy else None
     if prune is not None and static_s is not None and policy.layer_budget == "sparsity":
@@ -252,42 +258,68 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
     # The step before each prune round settles its own score update, so the
     # round reads no K row to apply it.
     fn_last = fn if args.no_settle else lib.lethe_decode_attn_score_final
+    fn_compact = lib.lethe_decode_attn_score_compact
     out_p, ws_p, wsb = ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel()
+    plan_p, planb = ctypes.c_void_p(ws_c.data_ptr()), ws_c.numel()
     q_ptr = [[ctypes.c_void_p(qp[t, l].data_ptr()) for l in range(Lyr)] for t in range(E * P)]
     k_ptr = [[ctypes.c_void_p(kp[t, l].data_ptr()) for l in range(Lyr)] for t in range(E * P)]
     v_ptr = [[ctypes.c_void_p(vp[t, l].data_ptr()) for l in range(Lyr)] for t in range(E * P)]
 
+    # Lengths once each interval's first step is done (with fused compaction
+    # that step drops the evicted rows), and at the end.
     len_snap = [torch.empty((Lyr, B), dtype=torch.int32, pin_memory=True) for _ in range(windows + 1)]
-    win_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(windows)]
+    # Events: interval start, after its first and second steps, end of its
+    # decode steps, after the budgets, after the selection, end of the round.
+    win_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(windows + 1)]
+    planned = [False]  # a compaction plan waits for the next step
+
+    def decode_step(t, f, compact):
+        for l in range(Lyr):
+            if compact:
+                rc = fn_compact(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, plan_p, planb,
+                                ws_p, wsb, sp)
+            else:
+                rc = f(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, ws_p, wsb, sp)
+            if rc != 0:
+                raise RuntimeError("decode call: %s" % L.status_string(rc))
 
     def run_window(w):
-        len_snap[w].copy_(cache.len, non_blocking=True)
-        win_ev[w][0].record(stream)
+        ev = win_ev[w]
+        ev[0].record(stream)
         for i in range(interval):
             tg = w * interval + i
             t = (min(tg // epoch, E - 1) * P if epoch else 0) + tg % P
-            f = fn_last if i == interval - 1 else fn
-            for l in range(Lyr):
-                rc = f(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, ws_p, wsb, sp)
-                if rc != 0:
-                    raise RuntimeError("lethe_decode_attn_score: %s" % L.status_string(rc))
-        win_ev[w][1].record(stream)
+            decode_step(t, fn_last if i == interval - 1 else fn, i == 0 and planned[0])
+            if i == 0:
+                planned[0] = False
+                ev[1].record(stream)
+                len_snap[w].copy_(cache.len, non_blocking=True)
+            elif i == 1:
+                ev[2].record(stream)
+        ev[3].record(stream)
         if policy_name == "shrink":
             L.score_flush(cache)
-            win_ev[w][2].record(stream)
+            ev[4].record(stream)
             L.segmented_shrink(cache, args.segments, args.tau, recent, sink, evict, None, keep)
-            win_ev[w][3].record(stream)
-            L.kv_compact(cache, keep, ws_c)
+            ev[5].record(stream)
+            if fused:
+                L.kv_compact_plan(cache, keep, ws_c)
+            else:
+                L.kv_compact(cache, keep, ws_c)
         else:
             if policy.window_fills:
                 r, sk = prune.budgets(int(per_layer_all[w].min()), recent)
             else:
                 r, sk = prune.budgets(per_layer_dev[w], recent)
-            win_ev[w][2].record(stream)
+            ev[4].record(stream)
             prune.select(r, sk)
-            win_ev[w][3].record(stream)
-            prune.compact()
-        win_ev[w][4].record(stream)
+            ev[5].record(stream)
+            if fused:
+                prune.plan(ws_c)
+            else:
+                prune.compact()
+        planned[0] = fused
+        ev[6].record(stream)
 
     log("warm-up: %d interval(s) of %d decode steps" % (warmup, interval))
     for w in range(warmup):
@@ -301,41 +333,62 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     len_snap[windows].copy_(cache.len)
+    if fused:
+        # The last round's compaction happens in the next step: two more
+        # steps (outside the timed run) give its cost.
+        ev = win_ev[windows]
+        ev[0].record(stream)
+        decode_step(0, fn, True)
+        ev[1].record(stream)
+        decode_step(1, fn, False)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        # Rows the last round kept: the lengths after those two steps, less them.
+        last_kept = int(cache.len.cpu().numpy().astype(np.int64).sum()) - 2 * Lyr * B
+    else:
+        last_kept = int(len_snap[windows].numpy().astype(np.int64).sum())
     status = int(cache.dev_status[0])
     if status != 0:
         raise RuntimeError("device status bits set: %d" % status)
     log("timed intervals done")
 
-    # Work accounting from the length snapshots (lengths at the start of each
-    # interval; every decode step appends one row before attending).
+    # Work accounting from the length snapshots (lengths after each
+    # interval's first step, which appended one row to the rows kept).
     elem = 2
     row_bytes = HK * (2 * D * elem + 8)               # K + V + score read/write, all KV heads
     fixed_bytes = B * HQ * D * (elem + 4) + 2 * B * HK * D * elem
+    kept0 = [len_snap[w].numpy().astype(np.int64) - 1 for w in range(windows)]  # rows before step 0
     tokens = 0
+    tokens_rest = 0  # steps 1 .. interval-1 only
     for w in range(warmup, windows):
-        n0 = len_snap[w].numpy().astype(np.int64)
+        n0 = kept0[w]
         tokens += interval * int(n0.sum()) + Lyr * B * interval * (interval + 1) // 2
+        tokens_rest += (interval - 1) * int(n0.sum()) + Lyr * B * ((interval * (interval + 1)) // 2 - 1)
     elapsed = t1 - t0
-    decode_ms = [win_ev[w][0].elapsed_time(win_ev[w][1]) for w in range(warmup, windows)]
-    prune_ms = [win_ev[w][1].elapsed_time(win_ev[w][4]) for w in range(warmup, windows)]
-    select_ms = [win_ev[w][2].elapsed_time(win_ev[w][3]) for w in range(warmup, windows)]
+    ms = lambda w, i, j: win_ev[w][i].elapsed_time(win_ev[w][j])
+    decode_ms = [ms(w, 0, 3) for w in range(warmup, windows)]
+    round_ms = [ms(w, 3, 6) for w in range(warmup, windows)]
+    select_ms = [ms(w, 4, 5) for w in range(warmup, windows)]
+    # What a fused compaction adds to the step that carries it out: that
+    # step's time less the next step's (one row longer, no compaction).
+    extra = [max(ms(w + 1, 0, 1) - ms(w + 1, 1, 2), 0.0) if fused else 0.0 for w in range(windows)]
+    prune_ms = [round_ms[i] + extra[warmup + i] for i in range(steps)]
     # Roofline of lethe_decode_attn_score: one kernel launch per call, back to
     # back on the launch stream; the events bracket every decode call of the
-    # timed intervals, so their span / calls is the average launch duration
-    # (the settling calls' second, small kernel included: one step in an
-    # interval).
-    n_calls = steps * interval * Lyr
-    avg_call_s = float(np.sum(decode_ms)) / 1e3 / n_calls
-    avg_call_bytes = (tokens * row_bytes + n_calls * fixed_bytes) / n_calls
+    # timed intervals after each interval's first step (which carries a fused
+    # compaction), so their span / calls is the average launch duration (the
+    # settling calls' second, small kernel included: one step in an interval).
+    n_calls = steps * (interval - 1) * Lyr
+    avg_call_s = float(np.sum([ms(w, 1, 3) for w in range(warmup, windows)])) / 1e3 / n_calls
+    avg_call_bytes = (tokens_rest * row_bytes + n_calls * fixed_bytes) / n_calls
     achieved = avg_call_bytes / avg_call_s / 1e9
     traffic = load_traffic(cfg_id, avg_call_bytes) if policy_name == "lethe" else None
 
     # Selection reads every live score once per KV head and writes a mask
-    # byte per row and head (lengths at the end of each interval, before
-    # compaction).
+    # byte per row and head (lengths at the end of each interval).
     sel_rows = 0
     for w in range(warmup, windows):
-        sel_rows += int(len_snap[w].numpy().astype(np.int64).sum()) + Lyr * B * interval
+        sel_rows += int(kept0[w].sum()) + Lyr * B * interval
     select_gbs = sel_rows * HK * 5 / (float(np.sum(select_ms)) / 1e3) / 1e9
 
     value = tokens / elapsed
@@ -343,10 +396,11 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
     # next interval: per-step decode time is fit as a + b * (cached tokens)
     # over every interval of the run (warm-up included), and round w saves
     # interval * b * (tokens it evicted).
-    all_dec = np.array([win_ev[w][0].elapsed_time(win_ev[w][1]) for w in range(windows)]) / interval
-    all_prune = np.array([win_ev[w][1].elapsed_time(win_ev[w][4]) for w in range(windows)])
-    start_rows = np.array([int(len_snap[w].numpy().astype(np.int64).sum()) for w in range(windows + 1)])
-    mid_rows = start_rows[:windows] + Lyr * B * (interval + 1) / 2.0
+    all_dec = np.array([ms(w, 1, 3) for w in range(windows)]) / (interval - 1)
+    all_prune = np.array([ms(w, 3, 6) + extra[w] for w in range(windows)])
+    start_rows = np.array([int(kept0[w].sum()) for w in range(windows)] +
+                          [int(len_snap[windows].numpy().astype(np.int64).sum())])
+    mid_rows = start_rows[:windows] + Lyr * B * (interval + 2) / 2.0
     prune_vs_saved = None
     # The fit needs intervals of clearly different sizes (a run that starts
     # at the steady state has none).
@@ -354,7 +408,11 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
         slope, icpt = np.polyfit(mid_rows, all_dec, 1)
         ratios = []
         for w in range(windows):
-            evicted = start_rows[w] + Lyr * B * interval - start_rows[w + 1]
+            # Rows the round after interval w dropped: the rows at its end less
+            # the rows the next interval starts from.
+            end_rows = start_rows[w] + Lyr * B * interval
+            nxt = start_rows[w + 1] if w + 1 < windows else last_kept
+            evicted = end_rows - nxt
             saved_ms = interval * slope * evicted
             ratios.append(float(all_prune[w] / saved_ms) if saved_ms > 0 else None)
         steady = [r for r in ratios[1:] if r is not None]
@@ -362,6 +420,7 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
             "round1": ratios[0], "steady_median": float(np.median(steady)) if steady else None,
             "per_round": ratios, "decode_ms_per_token_step": float(slope), "decode_step_fixed_ms": float(icpt),
             "prune_round_ms": [float(x) for x in all_prune],
+            "fused_step_extra_ms": [float(x) for x in extra],
         }
     workload = WORKLOADS[cfg_id]
     if policy_name == "lethe-shared":
@@ -395,6 +454,8 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
         },
         "decode_step_ms": float(np.mean(decode_ms)) / interval,
         "prune_round_us": float(np.mean(prune_ms)) * 1e3,
+        "prune_kernels_us": float(np.mean(round_ms)) * 1e3,
+        "compaction": args.compaction,
         "policy": policy_name,
         "settled_last_step": not args.no_settle,
         "select_us": float(np.mean(select_ms)) * 1e3,

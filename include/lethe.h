@@ -101,6 +101,7 @@ typedef struct {
 #define LETHE_OP_SELECT 2
 #define LETHE_OP_COMPACT 3
 #define LETHE_OP_DECODE_FINAL 4
+#define LETHE_OP_COMPACT_PLAN 5
 
 /*
  * Bytes of device workspace `op` needs for this cache (0 when none).  No
@@ -393,6 +394,51 @@ lethe_status lethe_segmented_shrink(const lethe_cache* cache, int32_t segments, 
  */
 lethe_status lethe_kv_compact(const lethe_cache* cache, const uint8_t* keep, void* ws,
                               size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Compaction carried out by the next decode step (the same result as
+ * lethe_kv_compact, with the moves riding on the reads that decode step does
+ * anyway, so the rows that move are read once instead of twice).
+ *
+ * lethe_kv_compact_plan records, for every segment (l, b, h) with n live rows
+ * and the keep mask `keep` (uint8 [num_layers][rows_per_layer], as for
+ * lethe_kv_compact), the rows kept and, per 32-row step, the rows kept before
+ * it and the step's keep mask, into `plan` (lethe_workspace_bytes(cache,
+ * LETHE_OP_COMPACT_PLAN) bytes: 16 bytes per segment and 8 per 32 rows of
+ * capacity).  It changes nothing in the cache; the decode state's tiling
+ * hints take the kept counts.  If the KV heads of an (l, b) keep different
+ * counts, LETHE_DEV_HEAD_MISMATCH is set and that sequence's plan is invalid;
+ * a bad layout sets LETHE_DEV_BAD_LAYOUT likewise.
+ *
+ * lethe_decode_attn_score_compact(..., plan, plan_bytes, ws, ws_bytes, ...)
+ * is then, for one layer, the compaction of that layer by the plan followed
+ * by the decode step of lethe_decode_attn_score (same arguments, ws of
+ * LETHE_OP_DECODE size): the kept rows move in order to the front of their
+ * segment (K, V and score bit for bit, a pending score update applied to the
+ * rows kept), the new row is appended after them, the attention and the score
+ * update run over the kept rows and the new one, and len becomes the rows
+ * kept plus the appended one.  Rows past the new len are unspecified.  A
+ * sequence whose len differs from the one the plan was made for, or whose
+ * plan is invalid, is skipped as a bad layout (LETHE_DEV_BAD_LAYOUT, out =
+ * NaN, nothing of it changes).  Call it once per layer with the plan made
+ * after the layer's last change; the plan must stay untouched until the last
+ * of them.
+ *
+ * Per segment, the rows from the first 32-row step holding an evicted row to
+ * the end are walked by one block, four steps at a time: once the block has
+ * read a group of steps, their kept rows go to their places, which lie at or
+ * before them and after every row the other blocks read.  bf16
+ * caches only (LETHE_ERR_UNSUPPORTED otherwise); step indices must fit int32
+ * (num_layers * (rows_per_layer / 32 + num_seqs * num_kv_heads) < 2^31) and
+ * num_kv_heads <= 64.  Errors: those of lethe_decode_attn_score, and
+ * LETHE_ERR_WORKSPACE for a plan buffer below the plan size.
+ */
+lethe_status lethe_kv_compact_plan(const lethe_cache* cache, const uint8_t* keep, void* plan, size_t plan_bytes,
+                                   hipStream_t stream);
+lethe_status lethe_decode_attn_score_compact(const lethe_cache* cache, int32_t layer, const void* q,
+                                             const void* k_new, const void* v_new, float gamma,
+                                             float softmax_scale, float* out, void* plan, size_t plan_bytes,
+                                             void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Apply the pending decode step of every (layer, sequence) to its scores

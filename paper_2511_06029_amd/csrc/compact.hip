@@ -433,6 +433,115 @@ int move_blocks() {
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Plan of a compaction that the next decode step carries out
+// ---------------------------------------------------------------------------
+// One block per (layer, sequence), one wavefront per KV head.  The wavefront
+// walks its segment's keep mask 64 rows at a time (16 loads a lane in
+// flight) and records, per 32-row step, the kept rows before the step and the
+// step's keep mask; it also finds the first step holding an evicted row and
+// clears the step flags the decode will set.  The block then checks that the
+// heads keep the same count (the new length is shared by the heads).
+constexpr int kPlanBatch = 16;  // 64-row groups a lane loads before it uses the first
+
+__device__ inline int wave_sum_i32(int v) {
+  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Heads a plan block holds counts for (host-checked).
+constexpr int kPlanMaxHeads = 64;
+
+__global__ __launch_bounds__(kWave * 8) void step_plan_kernel(PlanArgs a) {
+  const int lb = blockIdx.x;
+  const int l = lb / a.B;
+  const int b = lb - l * a.B;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int w = tid / kWave;
+  const int nw = blockDim.x / kWave;
+  __shared__ int s_kept[kPlanMaxHeads];
+  __shared__ int s_part[8];
+  // Steps of the earlier sequences of this layer: HK * ceil(cap / 32) each.
+  int part = 0;
+  for (int bb = tid; bb < b; bb += blockDim.x) part += (max(a.cap[bb], 0) + 31) >> 5;
+  part = wave_sum_i32(part);
+  if (lane == 0) s_part[w] = part;
+  __syncthreads();
+  long long before = 0;
+  for (int x = 0; x < nw; ++x) before += s_part[x];
+  const int n = a.len[lb];
+  const int c = a.cap[b];
+  const long long base = a.seq_base[b];
+  const int cs = (max(c, 0) + 31) >> 5;  // steps of one KV head's segment
+  // Segments that overlap (capacities summing past the layer) would run past
+  // the layer's steps: flagged like any other bad layout.
+  const bool bad = n < 0 || c < 0 || n > c || base < 0 || base + (long long)a.HK * c > a.rows_per_layer ||
+                   (before + cs) * a.HK > a.steps_per_layer;
+  for (int h = w; h < a.HK; h += nw) {
+    const long long step0 = (long long)l * a.steps_per_layer + before * a.HK + (long long)h * cs;
+    int kept = 0, t0 = 0;
+    if (!bad) {
+      const uint8_t* keep = a.keep + (long long)l * a.rows_per_layer + base + (long long)h * c;
+      const int nst = (n + 31) >> 5;
+      t0 = nst;
+      for (int j0 = 0; j0 < n; j0 += kPlanBatch * kWave) {
+        uint8_t kv[kPlanBatch];
+#pragma unroll
+        for (int u = 0; u < kPlanBatch; ++u) kv[u] = keep[min(j0 + u * kWave + lane, n - 1)];
+#pragma unroll
+        for (int u = 0; u < kPlanBatch; ++u) {
+          const int r0 = j0 + u * kWave;
+          if (r0 >= n) break;
+          const unsigned long long live = __ballot(r0 + lane < n);
+          const unsigned long long m = __ballot(r0 + lane < n && kv[u] != 0);
+          const unsigned long long ev = live & ~m;
+          if (ev != 0ull && t0 == nst) t0 = (r0 + (int)__builtin_ctzll(ev)) >> 5;
+          const long long t = step0 + (r0 >> 5);
+          const int lo = __popcll(m & 0xffffffffull);
+          if (lane == 0) {
+            a.step_plan[2 * t] = kept;
+            a.step_plan[2 * t + 1] = (int32_t)(uint32_t)m;
+            if (r0 + 32 < n) {
+              a.step_plan[2 * t + 2] = kept + lo;
+              a.step_plan[2 * t + 3] = (int32_t)(uint32_t)(m >> 32);
+            }
+          }
+          kept += __popcll(m);
+        }
+      }
+      for (int t = lane; t < nst; t += kWave) a.step_flag[step0 + t] = 0;
+    }
+    if (lane == 0) {
+      s_kept[h] = bad ? -1 : kept;
+      int32_t* sp = a.seg_plan + ((long long)lb * a.HK + h) * kSegPlanWords;
+      sp[0] = n;
+      sp[2] = t0;
+      sp[3] = (int32_t)step0;
+    }
+  }
+  __syncthreads();
+  bool same = true;
+  for (int x = 0; x < a.HK; ++x) same = same && s_kept[x] == s_kept[0];
+  const bool valid = !bad && same;
+  for (int h = tid; h < a.HK; h += blockDim.x)
+    a.seg_plan[((long long)lb * a.HK + h) * kSegPlanWords + 1] = valid ? s_kept[h] : -1;
+  if (tid == 0) {
+    if (bad) atomicOr(a.dev_status, LETHE_DEV_BAD_LAYOUT);
+    else if (!same) atomicOr(a.dev_status, LETHE_DEV_HEAD_MISMATCH);
+    a.hint[lb] = valid ? s_kept[0] : n;
+  }
+}
+
+lethe_status launch_plan(const PlanArgs& a, hipStream_t s) {
+  const long long nb = (long long)a.L * a.B;
+  if (nb > 0x7fffffffLL) return LETHE_ERR_UNSUPPORTED;
+  if (a.HK > kPlanMaxHeads) return LETHE_ERR_UNSUPPORTED;
+  const int waves = a.HK < 8 ? a.HK : 8;
+  hipLaunchKernelGGL(step_plan_kernel, dim3((unsigned)nb), dim3(kWave * waves), 0, s, a);
+  return hipGetLastError() == hipSuccess ? LETHE_OK : LETHE_ERR_HIP;
+}
+
 lethe_status launch_compact(const CompactArgs& args, hipStream_t s) {
   static const int spin_limit = env_int("LETHE_COMPACT_SPIN_LIMIT", kSpinLimit);
   static const int test_wait = env_int("LETHE_COMPACT_TEST_WAIT", 0);

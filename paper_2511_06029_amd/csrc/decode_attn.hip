@@ -77,14 +77,41 @@ __device__ inline float2 ld_agent2(const float* p) {
 // What one block works on.
 struct Chunk {
   int b, h, seg, c;
-  int ncache;        // rows already in the cache; the appended row is row ncache
+  int ncache;        // rows already in the cache (read by this call)
+  int dst_app;       // where the appended row goes (ncache, or the rows kept)
   bool app;          // a row is appended to this sequence
   long long segrow0; // first row of the segment in the layer
   int32_t* next;     // the segment's step counter
   int first, stride; // wave w's first step is first + w; then first + w + stride, ...
                      // (stride 0: from the counter, whose n-th reply is step dyn_base + n)
   int dyn_base;
+  int t0;            // compacting call: first step holding an evicted row
+  int step0;         // compacting call: index of step 0 in the plan's step arrays
 };
+
+// Compacting call: waits until the plan steps [lo, hi] (absolute indices)
+// have been read, one lane per step; `ready` (bit k: step spec0 + k was seen
+// read already) spares the polls of steps known to be done.  Every lane polls
+// at most spin_limit times over the call; past that the call gives up
+// waiting and reports LETHE_DEV_WAIT_TIMEOUT.
+__device__ inline void wait_steps(const DecodeArgs& a, int lo, int hi, int spec0, uint32_t ready, int& spins) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int t = lo + lane;
+  const int k = t - spec0;
+  bool wait = t <= hi && !(k >= 0 && k < 32 && ((ready >> k) & 1u));
+  while (wait) {
+    wait = __hip_atomic_load(&a.step_flag[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0;
+    if (wait) {
+      if (++spins > a.spin_limit) {
+        atomicOr(a.dev_status, LETHE_DEV_WAIT_TIMEOUT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  // The stores that follow stay after the wait.
+  asm volatile("" ::: "memory");
+}
 
 // A wavefront's steps after its first (which is fixed, so its loads need no
 // round trip): from the segment's counter (whichever wave asks first), or
@@ -170,7 +197,7 @@ __device__ void finish_single(const DecodeArgs& a, const Chunk& ck, const Combin
       o0 += cb.o[k][g][d] * f;
       o1 += cb.o[k][g][d + 1] * f;
     }
-    const float inv = 1.0f / lsum;
+    const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;  // no row attended: out = 0
     *reinterpret_cast<float2*>(outb + g * D + d) = make_float2(o0 * inv, o1 * inv);
     if (d == 0) {
       stat[g] = mx;
@@ -215,7 +242,7 @@ __device__ void combine_segment(const DecodeArgs& a, const Chunk& ck, const floa
       }
       M = bm;
     }
-    const float inv = 1.0f / lsum;
+    const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;  // no row attended: out = 0
     *reinterpret_cast<float2*>(outb + g * D + d) = make_float2(o0 * inv, o1 * inv);
     if (d == 0) {
       stat[g] = M;
@@ -263,7 +290,7 @@ __device__ inline bf16x8_t q_operand(const char* qgroup, int s, int g4, int kk) 
                  : zero_bf16x8();
 }
 
-template <int D, int G, class ReadPending>
+template <int D, int G, bool kCompact, class ReadPending>
 __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const ReadPending& read_pending,
                                 char* vtiles, CombineLds& cb) {
   using Cfg = MfmaCfg<D>;
@@ -296,6 +323,13 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
   // The first step is fixed, so its loads leave before anything else is read.
   bf16x8_t kr[2][KK];
   float sold = 0.0f;
+  // Compacting call, steps from t0 on (those holding rows that move): the
+  // plan entry of the step (rows kept before it, keep mask of its rows), and
+  // a first look at the flags of the 8 steps before it (lane k < 8: step
+  // t - 8 + k; steps before t0 never move and count as read).
+  int npre = 0;
+  uint32_t nmask = ~0u;
+  int nflag = 1;
   auto load_k = [&](int bs) {
 #pragma unroll
     for (int T = 0; T < 2; ++T) {
@@ -305,6 +339,18 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
         kr[T][kk] = *reinterpret_cast<const bf16x8_t*>(Kb + (long long)row * ROWB + 64 * kk + 16 * g4);
     }
     sold = g4 < 2 ? sseg[min(bs + 16 * g4 + s, re - 1)] : 0.0f;
+    if constexpr (kCompact) {
+      const int t = bs / STEP;
+      if (t >= ck.t0) {  // wave-uniform
+        const int2 e = *reinterpret_cast<const int2*>(a.step_plan + 2 * ((long long)ck.step0 + t));
+        npre = e.x;
+        nmask = (uint32_t)e.y;
+        const int tf = t - 8 + lane;
+        nflag = (lane < 8 && tf >= ck.t0)
+                    ? __hip_atomic_load(&a.step_flag[ck.step0 + tf], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                    : 1;
+      }
+    }
   };
   auto load_v = [&](int bs) {
 #pragma unroll
@@ -314,12 +360,18 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
                                        (lds_void_t*)((lds_char_t*)vb + u * Cfg::VBLK), 16, 0, 0);
     }
   };
+  int fixed_next = ck.first + w + ck.stride;
+  // A wave's first step is fixed, except in a compacting call where that
+  // step would hold rows that move: every such step comes from the counter,
+  // in row order, so a wave waits only for steps claimed before its own, by
+  // running waves.
   int idx = ck.first + w;
-  int fixed_next = idx + ck.stride;
+  if (kCompact && idx >= ck.dyn_base) idx = step_index(step_request(ck, fixed_next, lane));
   if (idx < nsteps) {
     load_k(idx * STEP);
     load_v(idx * STEP);
   }
+  int spins = 0;  // flag polls of this lane (compacting call)
 
   const Pending<G> pd = read_pending();
   const int pre_end = min(pd.rows, re);
@@ -345,18 +397,19 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
   f32x4_t o[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-
   const float sc = a.scale_log2;
-  int nidx = nsteps + 1;
-  int graw = idx < nsteps ? step_request(ck, fixed_next, lane) : 0;
-  while (idx < nsteps) {
-    const int base = idx * STEP;
-    nidx = step_index(graw);
-    const bool more = nidx < nsteps;  // wave-uniform
+
+  // One 32-row step whose K is in kr, its V in the wave's LDS tile and its
+  // old scores in sold.  `moving` (compacting call, steps from t0 on): only
+  // the rows of `cmask` take part, and the kept rows go to rows cpre, cpre +
+  // 1, ... of the segment once the steps holding those rows have been read
+  // (cready: which of the 8 steps before this one were seen read already).
+  // after_k runs once kr is free, after_v once the V tile is.
+  auto step = [&](int base, bool moving, int cpre, uint32_t cmask, uint32_t cready, auto&& after_k,
+                  auto&& after_v) {
     const bool pstep = base < pre_end;
     const int prow = base + 16 * g4 + s;
     const bool pon = pstep && g4 < 2 && prow < pre_end;
-
     f32x4_t sacc[2];
 #pragma unroll
     for (int T = 0; T < 2; ++T) {
@@ -375,6 +428,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
         if (g4 < 2 && row < re) *reinterpret_cast<f32x4_t*>(xlog + (long long)row * kLogitStride + 4 * g4) = sx;
       }
     }
+    float pval = 0.0f;  // the row's score after the pending update (pon)
     if (pstep) {
       // S = Q_prev K^T: lane (g4, s) gets heads 4 g4 + rr of row 16 T + s.
       float part[2];
@@ -389,9 +443,57 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
         for (int rr = 0; rr < 4; ++rr) acc = fmaf(hw_exp2(fmaf(so[rr], pd.scale, -pm[rr])), pi[rr], acc);
         part[T] = acc + __shfl_xor(acc, 16);
       }
-      if (pon) pd.score[prow] = fmaf(pd.gamma, sold, g4 == 0 ? part[0] : part[1]);
+      pval = fmaf(pd.gamma, sold, g4 == 0 ? part[0] : part[1]);
+      if (pon && !moving) pd.score[prow] = pval;
     }
-    if (more) load_k(nidx * STEP);
+    if constexpr (kCompact) {
+      if (moving) {
+        // The kept rows go to rows cpre .. cpre + kept - 1: the earlier steps
+        // holding those rows must have been read.
+        const int kc = __popc(cmask);
+        const int t = base / STEP;
+        if (kc > 0) {
+          const int lo = max(cpre / STEP, ck.t0), hi = min((cpre + kc - 1) / STEP, t - 1);
+          if (lo <= hi) wait_steps(a, ck.step0 + lo, ck.step0 + hi, ck.step0 + t - 8, cready, spins);
+        }
+        // Kept rows to their places: K from the operand registers (lane
+        // (g4, s) holds bytes 64 kk + 16 g4 of row 16 T + s), V from the LDS
+        // tile (16 bytes a lane), scores with the pending update where due.
+        char* Kw = reinterpret_cast<char*>(a.k_w) + ck.segrow0 * ROWB;
+        char* Vw = reinterpret_cast<char*>(a.v_w) + ck.segrow0 * ROWB;
+        auto dst_of = [&](int r) { return cpre + __popc(cmask & ((1u << r) - 1u)); };
+#pragma unroll
+        for (int T = 0; T < 2; ++T) {
+          const int r = 16 * T + s;
+          const int dst = dst_of(r);
+          if (((cmask >> r) & 1u) && dst != base + r && dst < ck.dst_app) {
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk)
+              *reinterpret_cast<bf16x8_t*>(Kw + (long long)dst * ROWB + 64 * kk + 16 * g4) = kr[T][kk];
+          }
+        }
+        constexpr int CPR = ROWB / 16;    // 16-byte pieces per row
+        constexpr int RPP = kWave / CPR;  // rows per pass
+        const int piece = lane % CPR;
+#pragma unroll 1
+        for (int i = 0; i < STEP / RPP; ++i) {
+          const int r = lane / CPR + RPP * i;
+          const int dst = dst_of(r);
+          if (((cmask >> r) & 1u) && dst != base + r && dst < ck.dst_app) {
+            typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+            typedef __attribute__((address_space(3))) const u32x4_t lds_u32x4_t;
+            const u32x4_t v = *reinterpret_cast<lds_u32x4_t*>((lds_char_t*)vb + Cfg::vaddr(r, 16 * piece));
+            *reinterpret_cast<u32x4_t*>(Vw + (long long)dst * ROWB + 16 * piece) = v;
+          }
+        }
+        if (g4 < 2) {
+          const int r = 16 * g4 + s;
+          const int dst = dst_of(r);
+          if (((cmask >> r) & 1u) && (dst != prow || pon) && dst < ck.dst_app) sseg[dst] = pon ? pval : sold;
+        }
+      }
+    }
+    after_k();
 
     // Logits of rows base + 16 T + 4 g4 + rr for head s.
     float x[2][4];
@@ -401,7 +503,8 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int row = base + 16 * T + 4 * g4 + rr;
-        x[T][rr] = row < re ? sacc[T][rr] * sc : -INFINITY;
+        const bool live = row < re && (!kCompact || !moving || ((cmask >> (16 * T + 4 * g4 + rr)) & 1u));
+        x[T][rr] = live ? sacc[T][rr] * sc : -INFINITY;
         mx = fmaxf(mx, x[T][rr]);
       }
     }
@@ -438,26 +541,58 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
       o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ph, o[nt], 0, 0, 0);
       o[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pl, o[nt], 0, 0, 0);
     }
-    if (more) {
-      load_v(nidx * STEP);
-      graw = step_request(ck, fixed_next, lane);
+    after_v();
+  };
+
+  int nidx = nsteps + 1;
+  int graw = idx < nsteps ? step_request(ck, fixed_next, lane) : 0;
+  while (idx < nsteps) {
+    const int base = idx * STEP;
+    nidx = step_index(graw);
+    const bool more = nidx < nsteps;  // wave-uniform
+    const bool moving = kCompact && idx >= ck.t0;
+    uint32_t cready = 0;
+    if constexpr (kCompact) {
+      if (moving) {
+        // Every load of this step has arrived (the reply to the claim above
+        // came after them): its rows may now be overwritten.
+        __builtin_amdgcn_s_waitcnt(0);
+        asm volatile("" ::: "memory");
+        if (lane == 0) __hip_atomic_store(&a.step_flag[ck.step0 + idx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        cready = (uint32_t)(__ballot(lane < 8 && nflag != 0) & 0xffull);
+      }
     }
+    step(base, moving, npre, nmask, cready, [&]() {
+      if (more) load_k(nidx * STEP);
+    }, [&]() {
+      if (more) {
+        load_v(nidx * STEP);
+        graw = step_request(ck, fixed_next, lane);
+      }
+    });
     idx = nidx;
   }
 
-  // The appended row (last chunk of its segment), by wave 0: read from
-  // k_new / v_new, copied into the cache, its score started at 0, and folded
-  // into wave 0's state.
+  // The appended row, by the wave that drew the step index equal to the
+  // step count: read from k_new / v_new, copied into the cache, its score
+  // started at 0, and folded into the wave's state.
   if (ck.app && idx == nsteps) {
     const char* kn = reinterpret_cast<const char*>(a.k_new) + (((long long)ck.b * a.HK + ck.h) * D) * 2;
     const char* vn = reinterpret_cast<const char*>(a.v_new) + (((long long)ck.b * a.HK + ck.h) * D) * 2;
+    if constexpr (kCompact) {
+      // The new row's place held an old row until this call read it.
+      if (ck.dst_app < re) {
+        const int t = ck.dst_app / STEP;
+        wait_steps(a, ck.step0 + t, ck.step0 + t, 0, 0u, spins);
+      }
+    }
     if (lane < LPR) {
-      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.k_w) + (ck.segrow0 + ck.ncache) * ROWB + 16 * lane) =
+      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.k_w) + (ck.segrow0 + ck.dst_app) * ROWB + 16 * lane) =
           *reinterpret_cast<const uint4*>(kn + 16 * lane);
-      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.v_w) + (ck.segrow0 + ck.ncache) * ROWB + 16 * lane) =
+      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.v_w) + (ck.segrow0 + ck.dst_app) * ROWB + 16 * lane) =
           *reinterpret_cast<const uint4*>(vn + 16 * lane);
     }
-    if (lane == 0) pd.score[ck.ncache] = 0.0f;
+    if (lane == 0) pd.score[ck.dst_app] = 0.0f;
     if (xlog) {
       // The appended row's logits as a cached row would give them: every
       // column of the B operand is k_new.
@@ -841,7 +976,7 @@ __device__ inline BlockPlan plan_block(const DecodeArgs& a, int blk, SeqWords& w
   return p;
 }
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool kCompact>
 __device__ inline void decode_body(const DecodeArgs& a) {
   __shared__ __attribute__((aligned(16))) AttnLds<T, D> S;
   __shared__ int s_last;
@@ -881,11 +1016,26 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   const int cp = sw.cp;
   const long long sbase = sw.sbase;
   const bool app = a.k_new != nullptr;
-  const bool bad = n < 0 || cp < 0 || n > cp || sbase < 0 || sbase + (long long)a.HK * cp > a.rows_per_layer;
-  const bool ovf = !bad && app && n >= cp;
-  const int n_att = (bad || ovf) ? 0 : n + (app ? 1 : 0);
+  // Compacting call: the plan of this segment; the rows it keeps replace the
+  // cached ones (a plan made for other lengths, or invalid, skips the
+  // sequence as a bad layout would).
+  int n_keep = n, t0 = 0, step0 = 0;
+  bool plan_ok = true;
+  if constexpr (kCompact) {
+    const int32_t* sp = a.seg_plan + (long long)seg * kSegPlanWords;
+    n_keep = sp[1];
+    t0 = sp[2];
+    step0 = sp[3];
+    plan_ok = sp[0] == n && n_keep >= 0 && n_keep <= n && t0 >= 0 && t0 <= (n + 31) / 32 && step0 >= 0 &&
+              (long long)step0 + (n + 31) / 32 <= a.plan_steps;
+  }
+  const bool bad = n < 0 || cp < 0 || n > cp || sbase < 0 || sbase + (long long)a.HK * cp > a.rows_per_layer ||
+                   !plan_ok;
+  const bool ovf = !bad && app && n_keep >= cp;
+  const int n_att = (bad || ovf) ? 0 : n_keep + (app ? 1 : 0);
   const bool settle = a.logit != nullptr;
-  if (n_att == 0) {
+  // (A compacting call that keeps no row still publishes the new length.)
+  if (n_att == 0 && (!kCompact || bad || ovf)) {
     // Skipped (flagged) or empty sequence: its out rows get NaN or 0, nothing
     // else of it changes, and no counter is touched.
     if (c == 0) {
@@ -908,10 +1058,15 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   ck.c = c;
   ck.next = &a.seg_cnt[(long long)seg * kCntStride + kStepCounter];
   ck.first = c * kNumWaves;  // wave w starts at step c * waves + w
-  ck.stride = a.deterministic ? nch * kNumWaves : 0;
-  ck.dyn_base = nch * kNumWaves;
+  ck.stride = (a.deterministic && !kCompact) ? nch * kNumWaves : 0;
+  // A compacting call fixes first steps only below t0 (rows that stay); the
+  // counter hands out every step from there on.
+  ck.dyn_base = kCompact ? min(nch * kNumWaves, t0) : nch * kNumWaves;
   ck.app = app;
   ck.ncache = n;
+  ck.dst_app = n_keep;
+  ck.t0 = t0;
+  ck.step0 = step0;
   ck.segrow0 = sbase + (long long)h * cp;
   const int ps = part_stride(G, D);
 
@@ -936,7 +1091,7 @@ __device__ inline void decode_body(const DecodeArgs& a) {
   auto read_pending = [&]() { return pd0; };
   auto publish = [&](int seen) {
     if (seen != seq_full) return;
-    if (app) a.len[b] = n_att;
+    if (app || kCompact) a.len[b] = n_att;
     // A settling call leaves nothing pending: its second launch applies the
     // step to the n_att rows.
     a.pend_len[b] = settle ? 0 : n_att;
@@ -949,7 +1104,7 @@ __device__ inline void decode_body(const DecodeArgs& a) {
 
   {
     if constexpr (sizeof(T) == 2)
-      attn_chunk_mfma<D, G>(a, ck, read_pending, S.vtiles, S.cb);
+      attn_chunk_mfma<D, G, kCompact>(a, ck, read_pending, S.vtiles, S.cb);
     else
       attn_chunk_f32<D, G>(a, ck, read_pending, S.cb);
     // Both routines end with a barrier that every wave reaches after its
@@ -994,17 +1149,27 @@ __device__ inline void decode_body(const DecodeArgs& a) {
 // bf16: three resident blocks per CU need at most 168 registers per lane.
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void decode_bf16_kernel(DecodeArgs a) {
-  decode_body<bf16_t, D, G>(a);
+  decode_body<bf16_t, D, G, false>(a);
+}
+
+// The compacting step (one call per layer and prune round): the same three
+// resident blocks per CU.
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void decode_bf16_compact_kernel(
+    DecodeArgs a) {
+  decode_body<bf16_t, D, G, true>(a);
 }
 
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) void decode_f32_kernel(DecodeArgs a) {
-  decode_body<float, D, G>(a);
+  decode_body<float, D, G, false>(a);
 }
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool kCompact>
 constexpr auto decode_kernel() {
-  if constexpr (sizeof(T) == 2)
+  if constexpr (sizeof(T) == 2 && kCompact)
+    return decode_bf16_compact_kernel<D, G>;
+  else if constexpr (sizeof(T) == 2)
     return decode_bf16_kernel<D, G>;
   else
     return decode_f32_kernel<D, G>;
@@ -1250,7 +1415,7 @@ int env_int(const char* name) {
 constexpr int64_t kRowsPerTargetChunk = 2048;
 constexpr int64_t kMinTarget = 512, kMaxTarget = 2048;
 
-template <typename T, int D, int G>
+template <typename T, int D, int G, bool kCompact = false>
 lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   DecodeArgs a = a_in;
   const int env_blocks = env_int("LETHE_DECODE_BLOCKS");
@@ -1280,7 +1445,7 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   a.nch_flat = (int32_t)nflat;
   int64_t grid = nbt + segs;
   if (grid < segs * nflat) grid = segs * nflat;
-  const auto kernel = decode_kernel<T, D, G>();
+  const auto kernel = decode_kernel<T, D, G, kCompact>();
   hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kThreads), 0, s, a);
   if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
   if (a.logit) {
@@ -1293,6 +1458,21 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
     if (hipGetLastError() != hipSuccess) return LETHE_ERR_HIP;
   }
   return LETHE_OK;
+}
+
+template <int D>
+lethe_status launch_compact_d(const DecodeArgs& a, int G, hipStream_t s) {
+  switch (G) {
+    case 1: return launch_tdg<bf16_t, D, 1, true>(a, s);
+    case 2: return launch_tdg<bf16_t, D, 2, true>(a, s);
+    case 3: return launch_tdg<bf16_t, D, 3, true>(a, s);
+    case 4: return launch_tdg<bf16_t, D, 4, true>(a, s);
+    case 5: return launch_tdg<bf16_t, D, 5, true>(a, s);
+    case 6: return launch_tdg<bf16_t, D, 6, true>(a, s);
+    case 7: return launch_tdg<bf16_t, D, 7, true>(a, s);
+    case 8: return launch_tdg<bf16_t, D, 8, true>(a, s);
+  }
+  return LETHE_ERR_UNSUPPORTED;
 }
 
 template <typename T, int D>
@@ -1366,6 +1546,12 @@ lethe_status launch_decode(const DecodeArgs& a, lethe_dtype dt, int D, int G, hi
     if (D == 128) return launch_td<float, 128>(a, G, s);
     if (D == 64) return launch_td<float, 64>(a, G, s);
   }
+  return LETHE_ERR_UNSUPPORTED;
+}
+
+lethe_status launch_decode_compact(const DecodeArgs& a, int D, int G, hipStream_t s) {
+  if (D == 128) return launch_compact_d<128>(a, G, s);
+  if (D == 64) return launch_compact_d<64>(a, G, s);
   return LETHE_ERR_UNSUPPORTED;
 }
 

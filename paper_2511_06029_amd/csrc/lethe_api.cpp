@@ -2,6 +2,7 @@
 // dispatch.  Every check here runs before any HIP call, so invalid calls
 // return without touching the device.
 #include <math.h>
+#include <stdlib.h>
 
 #include "compact_internal.h"
 #include "lethe_internal.h"
@@ -98,6 +99,8 @@ size_t lethe_workspace_bytes(const lethe_cache* c, int op) {
       return 0;
     case LETHE_OP_COMPACT:
       return compact_ws_bytes(c->rows_per_layer, c->num_layers, c->num_seqs, c->num_kv_heads);
+    case LETHE_OP_COMPACT_PLAN:
+      return plan_ws_bytes(c->rows_per_layer, c->num_layers, c->num_seqs, c->num_kv_heads);
   }
   return 0;
 }
@@ -130,12 +133,11 @@ lethe_status check_decode(const lethe_cache* c, int32_t layer, const void* q, co
   return LETHE_OK;
 }
 
-// A decode call whose arguments passed check_decode; ws holds at least one
-// chunk partial per segment (and, settling, the logits after the partials
-// of a full workspace).
-lethe_status decode_call(const lethe_cache* c, int32_t layer, const void* q, const void* k_new,
-                         const void* v_new, float gamma, float softmax_scale, float* out, void* ws,
-                         size_t ws_bytes, bool settle, hipStream_t stream) {
+// Launch arguments of a decode call whose arguments passed check_decode; ws
+// holds at least one chunk partial per segment (and, settling, the logits
+// after the partials of a full workspace).
+DecodeArgs decode_args(const lethe_cache* c, int32_t layer, const void* q, const void* k_new, const void* v_new,
+                       float gamma, float softmax_scale, float* out, void* ws, size_t ws_bytes, bool settle) {
   const int G = group_size(c);
   const int D = c->head_dim;
   float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / sqrtf((float)D);
@@ -180,7 +182,55 @@ lethe_status decode_call(const lethe_cache* c, int32_t layer, const void* q, con
   a.deterministic = 0;
   a.logit = settle ? (float*)((char*)ws + decode_final_logit_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
   a.apply_rows = settle ? (int32_t*)((char*)ws + decode_final_rows_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
-  return launch_decode(a, c->dtype, D, G, stream);
+  a.seg_plan = nullptr;
+  a.step_plan = nullptr;
+  a.step_flag = nullptr;
+  a.plan_steps = 0;
+  a.spin_limit = 0;
+  return a;
+}
+
+lethe_status decode_call(const lethe_cache* c, int32_t layer, const void* q, const void* k_new,
+                         const void* v_new, float gamma, float softmax_scale, float* out, void* ws,
+                         size_t ws_bytes, bool settle, hipStream_t stream) {
+  const DecodeArgs a = decode_args(c, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, ws_bytes, settle);
+  return launch_decode(a, c->dtype, c->head_dim, group_size(c), stream);
+}
+
+// Where the parts of a compaction plan sit in its buffer.
+struct PlanParts {
+  int32_t* seg;
+  int32_t* step;
+  int32_t* flag;
+  int64_t steps_per_layer;
+};
+
+PlanParts plan_parts(const lethe_cache* c, void* plan) {
+  PlanParts p;
+  char* w = (char*)plan;
+  p.seg = (int32_t*)w;
+  w += plan_seg_bytes(c->num_layers, c->num_seqs, c->num_kv_heads);
+  p.step = (int32_t*)w;
+  w += plan_step_bytes(c->rows_per_layer, c->num_layers, c->num_seqs, c->num_kv_heads);
+  p.flag = (int32_t*)w;
+  p.steps_per_layer = plan_steps_per_layer(c->rows_per_layer, c->num_seqs, c->num_kv_heads);
+  return p;
+}
+
+// Bounded waits of the compacting decode: 2^20 flag polls per wavefront
+// (about a second); LETHE_COMPACT_SPIN_LIMIT lowers it (tests).
+int decode_spin_limit() {
+  const char* e = getenv("LETHE_COMPACT_SPIN_LIMIT");
+  const int v = e ? atoi(e) : 0;
+  return (v > 0 && v < (1 << 20)) ? v : (1 << 20);
+}
+
+// Host limits of a plan: step indices are int32, and a block counts the
+// heads of a (layer, sequence) in shared memory.
+lethe_status check_plan_size(const lethe_cache* c) {
+  const int64_t steps = plan_steps_per_layer(c->rows_per_layer, c->num_seqs, c->num_kv_heads) * c->num_layers;
+  if (steps > 0x7fffffffLL || c->num_kv_heads > 64) return LETHE_ERR_UNSUPPORTED;
+  return LETHE_OK;
 }
 
 }  // namespace
@@ -427,6 +477,58 @@ lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* w
   a.hint = (int32_t*)((char*)c->state + sl.hint_off);
   a.dev_status = c->dev_status;
   return launch_compact(a, stream);
+}
+
+lethe_status lethe_kv_compact_plan(const lethe_cache* c, const uint8_t* keep, void* plan, size_t plan_bytes,
+                                   hipStream_t stream) {
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  if (!keep || !plan) return LETHE_ERR_INVALID;
+  st = check_plan_size(c);
+  if (st != LETHE_OK) return st;
+  if (plan_bytes < plan_ws_bytes(c->rows_per_layer, c->num_layers, c->num_seqs, c->num_kv_heads))
+    return LETHE_ERR_WORKSPACE;
+  const PlanParts pp = plan_parts(c, plan);
+  PlanArgs a;
+  a.keep = keep;
+  a.len = c->len;
+  a.seq_base = c->seq_base;
+  a.cap = c->cap;
+  a.rows_per_layer = c->rows_per_layer;
+  a.L = c->num_layers;
+  a.B = c->num_seqs;
+  a.HK = c->num_kv_heads;
+  a.steps_per_layer = (int32_t)pp.steps_per_layer;
+  a.seg_plan = pp.seg;
+  a.step_plan = pp.step;
+  a.step_flag = pp.flag;
+  a.hint = (int32_t*)((char*)c->state + state_of(c).hint_off);
+  a.dev_status = c->dev_status;
+  return launch_plan(a, stream);
+}
+
+lethe_status lethe_decode_attn_score_compact(const lethe_cache* c, int32_t layer, const void* q,
+                                             const void* k_new, const void* v_new, float gamma,
+                                             float softmax_scale, float* out, void* plan, size_t plan_bytes,
+                                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  lethe_status st = check_decode(c, layer, q, k_new, v_new, gamma, softmax_scale, out);
+  if (st != LETHE_OK) return st;
+  if (c->dtype != LETHE_BF16) return LETHE_ERR_UNSUPPORTED;
+  st = check_plan_size(c);
+  if (st != LETHE_OK) return st;
+  if (!plan || !ws) return LETHE_ERR_INVALID;
+  if (plan_bytes < plan_ws_bytes(c->rows_per_layer, c->num_layers, c->num_seqs, c->num_kv_heads))
+    return LETHE_ERR_WORKSPACE;
+  if (ws_bytes < decode_ws_bytes(c->num_seqs, c->num_kv_heads, group_size(c), c->head_dim))
+    return LETHE_ERR_WORKSPACE;
+  DecodeArgs a = decode_args(c, layer, q, k_new, v_new, gamma, softmax_scale, out, ws, ws_bytes, false);
+  const PlanParts pp = plan_parts(c, plan);
+  a.seg_plan = pp.seg + (size_t)layer * c->num_seqs * c->num_kv_heads * kSegPlanWords;
+  a.step_plan = pp.step;
+  a.step_flag = pp.flag;
+  a.plan_steps = (int32_t)(pp.steps_per_layer * c->num_layers);
+  a.spin_limit = decode_spin_limit();
+  return launch_decode_compact(a, c->head_dim, group_size(c), stream);
 }
 
 }  // extern "C"

@@ -128,12 +128,59 @@ struct DecodeArgs {
   int32_t nbt;           // blocks the tiling aims for
   int32_t nch_flat;      // chunks per segment when every hint is 0
   int32_t deterministic; // fixed step schedule instead of the per-segment step counter
+  // Compacting call only (else null): the plan lethe_kv_compact_plan wrote.
+  const int32_t* seg_plan;  // this layer's [B*HK] x kSegPlanWords
+  const int32_t* step_plan; // [steps] x 2: kept rows before the step, keep mask of its 32 rows
+  int32_t* step_flag;       // [steps]: the step's rows have been read (set by this call)
+  int32_t plan_steps;       // steps the plan's arrays hold
+  int32_t spin_limit;       // flag polls a wavefront may spend in all
   // Settling call only (else null): the step's logits [rows_per_layer][8]
   // (raw q.k for bf16, scaled to log2 units for fp32) and the rows to
   // update per sequence (0: skipped), both in the workspace.
   float* logit;
   int32_t* apply_rows;
 };
+
+// Compaction that the next decode step carries out (lethe_kv_compact_plan,
+// lethe_decode_attn_score_compact).  Per (layer, sequence, KV head) segment
+// the plan keeps kSegPlanWords words: the live rows it was made for, the rows
+// kept (-1: no valid plan), the first 32-row step holding an evicted row, and
+// the index of the segment's step 0 in the per-step arrays.  Per step: the
+// kept rows before it, the keep mask of its 32 rows, and a flag the decode
+// sets once the step's rows have been read.  Steps of layer l start at
+// l * plan_steps_per_layer; those of sequence b after the steps of every
+// earlier sequence (ceil(cap / 32) per KV head).
+constexpr int kSegPlanWords = 4;
+inline int64_t plan_steps_per_layer(int64_t rows_per_layer, int B, int HK) {
+  return (rows_per_layer + 31) / 32 + (int64_t)B * HK;
+}
+inline size_t plan_seg_bytes(int L, int B, int HK) {
+  return align_up((size_t)L * B * HK * kSegPlanWords * sizeof(int32_t), 256);
+}
+inline size_t plan_step_bytes(int64_t rows_per_layer, int L, int B, int HK) {
+  return align_up((size_t)L * plan_steps_per_layer(rows_per_layer, B, HK) * 2 * sizeof(int32_t), 256);
+}
+inline size_t plan_ws_bytes(int64_t rows_per_layer, int L, int B, int HK) {
+  return plan_seg_bytes(L, B, HK) + plan_step_bytes(rows_per_layer, L, B, HK) +
+         align_up((size_t)L * plan_steps_per_layer(rows_per_layer, B, HK) * sizeof(int32_t), 256);
+}
+
+struct PlanArgs {
+  const uint8_t* keep;
+  const int32_t* len;
+  const int64_t* seq_base;
+  const int32_t* cap;
+  int64_t rows_per_layer;
+  int32_t L, B, HK;
+  int32_t steps_per_layer;
+  int32_t* seg_plan;
+  int32_t* step_plan;
+  int32_t* step_flag;
+  int32_t* hint;          // decode state [L][B]: set to the rows kept
+  int32_t* dev_status;
+};
+
+lethe_status launch_plan(const PlanArgs& a, hipStream_t s);
 
 struct FlushArgs {
   const void* k;         // all layers
@@ -156,6 +203,8 @@ struct FlushArgs {
 lethe_status launch_flush(const FlushArgs& a, lethe_dtype dt, int D, int G, hipStream_t s);
 
 lethe_status launch_decode(const DecodeArgs& a, lethe_dtype dt, int D, int G, hipStream_t s);
+// The decode step that also carries out the plan's compaction (bf16 only).
+lethe_status launch_decode_compact(const DecodeArgs& a, int D, int G, hipStream_t s);
 
 // Device scratch of lethe_decode_attn_score_noalloc: a static array of this
 // many bytes per device, holding the chunk partials of one call.

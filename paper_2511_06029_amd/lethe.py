@@ -14,12 +14,12 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblethe.so
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
 DEV_APPEND_OVERFLOW, DEV_INFEASIBLE, DEV_BAD_LAYOUT, DEV_HEAD_MISMATCH, DEV_WAIT_TIMEOUT = 1, 2, 4, 8, 16
-OP_DECODE, OP_SPARSITY, OP_SELECT, OP_COMPACT, OP_DECODE_FINAL = 0, 1, 2, 3, 4
+OP_DECODE, OP_SPARSITY, OP_SELECT, OP_COMPACT, OP_DECODE_FINAL, OP_COMPACT_PLAN = 0, 1, 2, 3, 4, 5
 
 SHRINK_NO_BREAKPOINT, SHRINK_NOT_TRIGGERED = -1, -2
 
 EXPORTED = ("lethe_workspace_bytes", "lethe_state_bytes", "lethe_decode_attn_score", "lethe_decode_attn_score_final",
-            "lethe_decode_attn_score_noalloc",
+            "lethe_decode_attn_score_noalloc", "lethe_kv_compact_plan", "lethe_decode_attn_score_compact",
             "lethe_layer_sparsity", "lethe_rasr_select", "lethe_rasr_select_shared",
             "lethe_segmented_shrink", "lethe_kv_compact", "lethe_score_flush",
             "lethe_prefill_attn_score", "lethe_prefill_workspace_bytes", "lethe_status_string")
@@ -83,6 +83,11 @@ def load():
         lib.lethe_prefill_workspace_bytes.restype = sz
         lib.lethe_kv_compact.argtypes = [pc, vp, vp, sz, vp]
         lib.lethe_kv_compact.restype = ctypes.c_int
+        lib.lethe_kv_compact_plan.argtypes = [pc, vp, vp, sz, vp]
+        lib.lethe_kv_compact_plan.restype = ctypes.c_int
+        lib.lethe_decode_attn_score_compact.argtypes = [pc, i32, vp, vp, vp, ctypes.c_float, ctypes.c_float, vp,
+                                                        vp, sz, vp, sz, vp]
+        lib.lethe_decode_attn_score_compact.restype = ctypes.c_int
         lib.lethe_status_string.argtypes = [ctypes.c_int]
         lib.lethe_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -209,6 +214,24 @@ def kv_compact(cache, keep, ws, stream=None):
     st = load().lethe_kv_compact(ctypes.byref(cache.c_struct()), _p(keep), _p(ws),
                                  ws.numel() * ws.element_size(), _stream(stream))
     _check("lethe_kv_compact", st)
+
+
+def kv_compact_plan(cache, keep, plan, stream=None):
+    """lethe_kv_compact_plan: record the compaction the next decode step of
+    each layer carries out (nothing in the cache changes)."""
+    st = load().lethe_kv_compact_plan(ctypes.byref(cache.c_struct()), _p(keep), _p(plan),
+                                      plan.numel() * plan.element_size(), _stream(stream))
+    _check("lethe_kv_compact_plan", st)
+
+
+def decode_attn_score_compact(cache, layer, q, k_new, v_new, gamma, softmax_scale, out, plan, ws, stream=None):
+    """lethe_decode_attn_score_compact: the layer's planned compaction, then
+    its decode step, in one call."""
+    st = load().lethe_decode_attn_score_compact(ctypes.byref(cache.c_struct()), int(layer), _p(q), _p(k_new),
+                                                _p(v_new), float(gamma), float(softmax_scale), _p(out), _p(plan),
+                                                plan.numel() * plan.element_size(), _p(ws),
+                                                ws.numel() * ws.element_size(), _stream(stream))
+    _check("lethe_decode_attn_score_compact", st)
 
 
 class LetheCache:

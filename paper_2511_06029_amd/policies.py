@@ -97,7 +97,7 @@ class PruneRound:
         self.budget = torch.empty((B, Ly), dtype=torch.int32, device=dev)
         self.keep = torch.empty((Ly, cache.rows_per_layer), dtype=torch.uint8, device=dev)
         self.gbud = torch.empty(B, dtype=torch.int64, device=dev)
-        self.ws = cache.workspace(L.OP_COMPACT)
+        self.ws = None  # compaction workspace, allocated by the first eager compaction
         s_in = policy.sparsity_in(Ly)
         self.s_in = None
         if s_in is not None:
@@ -144,7 +144,14 @@ class PruneRound:
             L.rasr_select(self.cache, self.budget, recent, sink, self.keep)
 
     def compact(self):
+        if self.ws is None:
+            self.ws = self.cache.workspace(L.OP_COMPACT)
         L.kv_compact(self.cache, self.keep, self.ws)
+
+    def plan(self, plan):
+        """The compaction as a plan the next decode step of each layer
+        carries out (lethe_decode_attn_score_compact)."""
+        L.kv_compact_plan(self.cache, self.keep, plan)
 
     def __call__(self, per_layer_budget, recent):
         r, sk = self.budgets(per_layer_budget, recent)
