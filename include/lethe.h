@@ -404,8 +404,9 @@ lethe_status lethe_kv_compact(const lethe_cache* cache, const uint8_t* keep, voi
  * and the keep mask `keep` (uint8 [num_layers][rows_per_layer], as for
  * lethe_kv_compact), the rows kept and, per 32-row step, the rows kept before
  * it and the step's keep mask, into `plan` (lethe_workspace_bytes(cache,
- * LETHE_OP_COMPACT_PLAN) bytes: 16 bytes per segment and 8 per 32 rows of
- * capacity).  It changes nothing in the cache; the decode state's tiling
+ * LETHE_OP_COMPACT_PLAN) bytes: 16 bytes per segment, and 12 per 32-row step
+ * of capacity plus one step per segment, for the step's kept-before count,
+ * mask and read flag).  It changes nothing in the cache; the decode state's tiling
  * hints take the kept counts.  If the KV heads of an (l, b) keep different
  * counts, LETHE_DEV_HEAD_MISMATCH is set and that sequence's plan is invalid;
  * a bad layout sets LETHE_DEV_BAD_LAYOUT likewise.
@@ -421,13 +422,19 @@ lethe_status lethe_kv_compact(const lethe_cache* cache, const uint8_t* keep, voi
  * sequence whose len differs from the one the plan was made for, or whose
  * plan is invalid, is skipped as a bad layout (LETHE_DEV_BAD_LAYOUT, out =
  * NaN, nothing of it changes).  Call it once per layer with the plan made
- * after the layer's last change; the plan must stay untouched until the last
- * of them.
+ * after the layer's last change; between the plan and the last of those
+ * calls only these calls may touch the plan (they set its step flags).
  *
- * Per segment, the rows from the first 32-row step holding an evicted row to
- * the end are walked by one block, four steps at a time: once the block has
- * read a group of steps, their kept rows go to their places, which lie at or
- * before them and after every row the other blocks read.  bf16
+ * The work split is lethe_decode_attn_score's: the wavefronts of a segment
+ * take its 32-row steps in increasing order.  From the first step holding
+ * an evicted row on, a wavefront marks its step read as soon as the step's
+ * loads have landed, and before storing the step's kept rows at their new
+ * places (at or before their old ones) waits for the steps those places lie
+ * in.  Those steps were taken earlier and are marked without waiting for
+ * anything, so every wait ends; each is still bounded (2^20 polls per
+ * wavefront, fewer if the environment variable LETHE_COMPACT_SPIN_LIMIT,
+ * read at each call, says so), and one that gives up sets
+ * LETHE_DEV_WAIT_TIMEOUT.  bf16
  * caches only (LETHE_ERR_UNSUPPORTED otherwise); step indices must fit int32
  * (num_layers * (rows_per_layer / 32 + num_seqs * num_kv_heads) < 2^31) and
  * num_kv_heads <= 64.  Errors: those of lethe_decode_attn_score, and
