@@ -98,10 +98,11 @@ def parse():
     ap.add_argument("--prefill", action="store_true", help="time the prompt prefill with score seeding instead")
     ap.add_argument("--no-settle", action="store_true",
                     help="last step of an interval deferred like the others (the prune round then applies it)")
-    ap.add_argument("--compaction", choices=("fused", "eager"), default="eager",
+    ap.add_argument("--compaction", choices=("fused", "eager", "overlap"), default="eager",
                     help="fused: the round plans the compaction and the next decode step of each layer carries it "
                          "out (lethe_kv_compact_plan + lethe_decode_attn_score_compact); eager: lethe_kv_compact "
-                         "in the round")
+                         "in the round; overlap: lethe_kv_compact_layers layer by layer on a second stream, each "
+                         "decode call of the next step waiting for its own layer's compaction")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="first copy MIB MiB device-to-device 3 times (counter calibration runs)")
     return ap.parse_args()
@@ -226,7 +227,21 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
     # with the deferred call's.
     ws = cache.workspace(L.OP_DECODE if args.no_settle else L.OP_DECODE_FINAL)
     fused = args.compaction == "fused"
+    overlap = args.compaction == "overlap"
+    deferred = fused or overlap  # the round's compaction lands in the next step
     ws_c = cache.workspace(L.OP_COMPACT_PLAN if fused else L.OP_COMPACT)
+    # overlap: the round compacts the layers on a side stream in groups of 1,
+    # 2, 4, ... layers; the next step's decode call of layer l waits for the
+    # group holding l only, so every group after the first runs beside the
+    # decode calls of the layers before it.
+    side = torch.cuda.Stream(device=dev) if overlap else None
+    sel_done = torch.cuda.Event() if overlap else None
+    groups = []
+    while sum(n for _, n in groups) < Lyr:
+        l0 = sum(n for _, n in groups)
+        groups.append((l0, min(1 << len(groups), Lyr - l0)))
+    group_done = [torch.cuda.Event() for _ in groups] if overlap else None
+    layer_done = [group_done[gi] for gi, (_, n) in enumerate(groups) for _ in range(n)] if overlap else None
     keep = torch.empty((Lyr, cache.rows_per_layer), dtype=torch.uint8, device=dev)
     prune = policies.PruneRound(cache, policy) if policy else None
     if prune is not None and static_s is not None and policy.layer_budget == "sparsity":
@@ -275,13 +290,22 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
 
     def decode_step(t, f, compact):
         for l in range(Lyr):
-            if compact:
+            if compact and overlap:
+                stream.wait_event(layer_done[l])
+            if compact and fused:
                 rc = fn_compact(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, plan_p, planb,
                                 ws_p, wsb, sp)
             else:
                 rc = f(cref, l, q_ptr[t][l], k_ptr[t][l], v_ptr[t][l], gamma, 0.0, out_p, ws_p, wsb, sp)
             if rc != 0:
                 raise RuntimeError("decode call: %s" % L.status_string(rc))
+
+    def compact_on_side(keep_t):
+        sel_done.record(stream)
+        side.wait_event(sel_done)
+        for gi, (l0, n) in enumerate(groups):
+            L.kv_compact_layers(cache, l0, n, keep_t, ws_c, stream=side)
+            group_done[gi].record(side)
 
     def run_window(w):
         ev = win_ev[w]
@@ -304,6 +328,8 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
             ev[5].record(stream)
             if fused:
                 L.kv_compact_plan(cache, keep, ws_c)
+            elif overlap:
+                compact_on_side(keep)
             else:
                 L.kv_compact(cache, keep, ws_c)
         else:
@@ -316,24 +342,31 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
             ev[5].record(stream)
             if fused:
                 prune.plan(ws_c)
+            elif overlap:
+                compact_on_side(prune.keep)
             else:
                 prune.compact()
-        planned[0] = fused
+        planned[0] = deferred
         ev[6].record(stream)
 
     log("warm-up: %d interval(s) of %d decode steps" % (warmup, interval))
+    # With overlapped compaction only the launch stream is waited for here:
+    # the side stream's work of the last round runs into the next interval
+    # and is charged to it, as a fused compaction is.
+    sync = stream.synchronize if overlap else torch.cuda.synchronize
     for w in range(warmup):
         run_window(w)
-    torch.cuda.synchronize()
+    sync()
     log("timed: %d interval(s)" % steps)
     t0 = time.perf_counter()
     for w in range(warmup, windows):
         run_window(w)
         log("interval %d enqueued" % w)
-    torch.cuda.synchronize()
+    sync()
     t1 = time.perf_counter()
-    len_snap[windows].copy_(cache.len)
-    if fused:
+    if not deferred:
+        len_snap[windows].copy_(cache.len)
+    if deferred:
         # The last round's compaction happens in the next step: two more
         # steps (outside the timed run) give its cost.
         ev = win_ev[windows]
@@ -344,7 +377,8 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
         ev[2].record(stream)
         torch.cuda.synchronize()
         # Rows the last round kept: the lengths after those two steps, less them.
-        last_kept = int(cache.len.cpu().numpy().astype(np.int64).sum()) - 2 * Lyr * B
+        len_snap[windows].copy_(cache.len - 2)
+        last_kept = int(len_snap[windows].numpy().astype(np.int64).sum())
     else:
         last_kept = int(len_snap[windows].numpy().astype(np.int64).sum())
     status = int(cache.dev_status[0])
@@ -369,9 +403,10 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
     decode_ms = [ms(w, 0, 3) for w in range(warmup, windows)]
     round_ms = [ms(w, 3, 6) for w in range(warmup, windows)]
     select_ms = [ms(w, 4, 5) for w in range(warmup, windows)]
-    # What a fused compaction adds to the step that carries it out: that
-    # step's time less the next step's (one row longer, no compaction).
-    extra = [max(ms(w + 1, 0, 1) - ms(w + 1, 1, 2), 0.0) if fused else 0.0 for w in range(windows)]
+    # What a fused or overlapped compaction adds to the step that carries it
+    # out (or runs beside it): that step's time less the next step's (one row
+    # longer, no compaction).
+    extra = [max(ms(w + 1, 0, 1) - ms(w + 1, 1, 2), 0.0) if deferred else 0.0 for w in range(windows)]
     prune_ms = [round_ms[i] + extra[warmup + i] for i in range(steps)]
     # Roofline of lethe_decode_attn_score: one kernel launch per call, back to
     # back on the launch stream; the events bracket every decode call of the

@@ -396,6 +396,22 @@ lethe_status lethe_kv_compact(const lethe_cache* cache, const uint8_t* keep, voi
                               size_t ws_bytes, hipStream_t stream);
 
 /*
+ * lethe_kv_compact restricted to layers layer_begin .. layer_begin +
+ * layer_count - 1 (the same result for those layers; nothing of the other
+ * layers is read or written, their rows of `keep` included).  A pending
+ * decode step of those layers is applied first.  Calls on one cache share the
+ * workspace and the queue counters in the decode state, so they must be
+ * ordered on one stream; a decode call of a layer outside the range may run
+ * concurrently on another stream, which lets a prune round compact layer l
+ * while the next decode step works on the layers before it (the decode call
+ * of layer l waits for its compaction).  layer_count 0 does nothing.  Errors:
+ * those of lethe_kv_compact, and LETHE_ERR_INVALID for a range outside
+ * 0 .. num_layers - 1.
+ */
+lethe_status lethe_kv_compact_layers(const lethe_cache* cache, int32_t layer_begin, int32_t layer_count,
+                                     const uint8_t* keep, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Compaction carried out by the next decode step (the same result as
  * lethe_kv_compact, with the moves riding on the reads that decode step does
  * anyway, so the rows that move are read once instead of twice).

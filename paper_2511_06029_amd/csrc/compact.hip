@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(CompactArgs 
   if (cidx < nseg) {
     const int h = (int)(cidx % a.HK);
     const int b = (int)((cidx / a.HK) % a.B);
-    const int l = (int)(cidx / ((long long)a.HK * a.B));
+    const int l = a.l0 + (int)(cidx / ((long long)a.HK * a.B));
     n = a.len[(long long)l * a.B + b];
     const int c = a.cap[b];
     const long long base = a.seq_base[b];
@@ -397,7 +397,8 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
   }
 }
 
-// New length of every (layer, sequence): the kept count, equal across heads.
+// New length of every (layer, sequence) of the call: the kept count, equal
+// across heads.
 // Also returns the queue counters to zero for the next call.
 __global__ void compact_len_kernel(CompactArgs a) {
   const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -414,8 +415,9 @@ __global__ void compact_len_kernel(CompactArgs a) {
   }
   if (mn < 0) return;  // bad layout, already flagged
   if (mn != mx) atomicOr(a.dev_status, LETHE_DEV_HEAD_MISMATCH);
-  a.len[i] = mn;
-  a.hint[i] = mn;
+  const long long lb = (long long)a.l0 * a.B + i;
+  a.len[lb] = mn;
+  a.hint[lb] = mn;
 }
 
 int env_int(const char* name, int dflt) {

@@ -56,10 +56,11 @@ struct CompactArgs {
   const int64_t* seq_base;
   const int32_t* cap;
   int64_t rows_per_layer;
-  int32_t L, B, HK;
+  int32_t l0;             // first layer of the call
+  int32_t L, B, HK;       // L: layers of the call (l0 .. l0 + L - 1)
   int32_t row_bytes;      // D * element size
   const uint8_t* keep;
-  int32_t* counts;        // ws [L][B][HK]
+  int32_t* counts;        // ws [L][B][HK] (the call's layers)
   CompactItem* items;     // ws [qcap]
   int32_t* flags;         // ws [qcap]: per tile, its rows are loaded
   int32_t qcap;           // tiles (and so entries) the queue holds at most; flags[qcap] is never set

@@ -312,7 +312,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
   float* const sseg = a.score + ck.segrow0;
   // Settling call: this step's S = Q K^T per row, in the orientation and
   // arithmetic of the deferred update.
-  float* const xlog = a.logit ? a.logit + ck.segrow0 * kLogitStride : nullptr;
+  float* const xlog = (!kCompact && a.logit) ? a.logit + ck.segrow0 * kLogitStride : nullptr;
 
   // Loads of a step: K rows into the operand registers and the old scores of
   // rows base + 16 g4 + s (lane groups 0 and 1, used if the pending update
@@ -325,11 +325,17 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
   float sold = 0.0f;
   // Compacting call, steps from t0 on (those holding rows that move): the
   // plan entry of the step (rows kept before it, keep mask of its rows), and
-  // a first look at the flags of the 8 steps before it (lane k < 8: step
-  // t - 8 + k; steps before t0 never move and count as read).
+  // a first look at the flags of the 8 steps before it (bit k: step t - 8 + k
+  // was seen read; steps before t0 never move and count as read).  Both are
+  // wave-uniform and come through the scalar cache, whose loads are counted
+  // apart from the vector memory operations: waiting for them never waits
+  // for the step's K and V loads or for earlier stores.  The plan does not
+  // change during the call; a flag only ever goes from 0 to 1 during it, so
+  // a stale scalar-cache copy can only under-report, which costs a poll in
+  // wait_steps and nothing else.
   int npre = 0;
   uint32_t nmask = ~0u;
-  int nflag = 1;
+  uint32_t nready = 0xffu;
   auto load_k = [&](int bs) {
 #pragma unroll
     for (int T = 0; T < 2; ++T) {
@@ -340,15 +346,22 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
     }
     sold = g4 < 2 ? sseg[min(bs + 16 * g4 + s, re - 1)] : 0.0f;
     if constexpr (kCompact) {
-      const int t = bs / STEP;
-      if (t >= ck.t0) {  // wave-uniform
-        const int2 e = *reinterpret_cast<const int2*>(a.step_plan + 2 * ((long long)ck.step0 + t));
-        npre = e.x;
-        nmask = (uint32_t)e.y;
-        const int tf = t - 8 + lane;
-        nflag = (lane < 8 && tf >= ck.t0)
-                    ? __hip_atomic_load(&a.step_flag[ck.step0 + tf], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                    : 1;
+      const int t = __builtin_amdgcn_readfirstlane(bs / STEP);
+      if (t >= ck.t0) {
+        typedef __attribute__((address_space(4))) const int32_t cint_t;
+        const cint_t* sp = (const cint_t*)(a.step_plan + 2 * ((long long)ck.step0 + t));
+        npre = sp[0];
+        nmask = (uint32_t)sp[1];
+        const cint_t* fl = (const cint_t*)(a.step_flag + ck.step0 + (t - 8));
+        nready = 0;
+        if (t - 8 >= ck.t0) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) nready |= (fl[k] != 0 ? 1u : 0u) << k;
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            if (t - 8 + k < ck.t0 || fl[k] != 0) nready |= 1u << k;
+        }
       }
     }
   };
@@ -559,7 +572,7 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
         __builtin_amdgcn_s_waitcnt(0);
         asm volatile("" ::: "memory");
         if (lane == 0) __hip_atomic_store(&a.step_flag[ck.step0 + idx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        cready = (uint32_t)(__ballot(lane < 8 && nflag != 0) & 0xffull);
+        cready = nready;
       }
     }
     step(base, moving, npre, nmask, cready, [&]() {
@@ -1243,8 +1256,8 @@ __device__ void flush_segment_valu(const FlushArgs& a, int lb, int h, int l, int
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
-  const int lb = blockIdx.x / a.HK;
-  const int h = blockIdx.x - lb * a.HK;
+  const int lb = a.l0 * a.B + (int)blockIdx.x / a.HK;
+  const int h = (int)blockIdx.x % a.HK;
   if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
   const int P = a.pend_len[lb];
   if (P <= 0) return;
@@ -1337,8 +1350,8 @@ __device__ void flush_segment_bf16(const FlushArgs& a, int lb, int h, int l, int
 
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
-  const int lb = blockIdx.x / a.HK;
-  const int h = blockIdx.x - lb * a.HK;
+  const int lb = a.l0 * a.B + (int)blockIdx.x / a.HK;
+  const int h = (int)blockIdx.x % a.HK;
   if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
   const int P = a.pend_len[lb];
   if (P <= 0) return;

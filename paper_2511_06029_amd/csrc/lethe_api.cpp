@@ -47,7 +47,9 @@ StateLayout state_of(const lethe_cache* c) {
 }
 
 // Applies every pending decode step (no-op kernel blocks where none is).
-lethe_status flush_pending(const lethe_cache* c, hipStream_t stream) {
+// Applies the pending decode step of layers l0 .. l0 + nl - 1 (all of them by
+// default) and refreshes their tiling hints.
+lethe_status flush_pending(const lethe_cache* c, hipStream_t stream, int l0 = 0, int nl = -1) {
   const StateLayout sl = state_of(c);
   char* st = (char*)c->state;
   FlushArgs a;
@@ -57,9 +59,11 @@ lethe_status flush_pending(const lethe_cache* c, hipStream_t stream) {
   a.seq_base = c->seq_base;
   a.cap = c->cap;
   a.rows_per_layer = c->rows_per_layer;
-  a.L = c->num_layers;
+  a.l0 = l0;
+  a.L = nl < 0 ? c->num_layers : nl;
   a.B = c->num_seqs;
   a.HK = c->num_kv_heads;
+  if ((long long)a.L * a.B * a.HK == 0) return LETHE_OK;
   a.pend_len = (int32_t*)(st + sl.len_off);
   a.pend_par = (const int32_t*)(st + sl.par_off);
   a.pend_gamma = (const float*)(st + sl.gamma_off);
@@ -440,13 +444,15 @@ lethe_status lethe_prefill_attn_score(const lethe_cache* c, int32_t layer, const
   return launch_prefill(a, D, G, stream);
 }
 
-lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* ws, size_t ws_bytes,
-                              hipStream_t stream) {
+lethe_status lethe_kv_compact_layers(const lethe_cache* c, int32_t layer_begin, int32_t layer_count,
+                                     const uint8_t* keep, void* ws, size_t ws_bytes, hipStream_t stream) {
   lethe_status st = check_cache(c);
   if (st != LETHE_OK) return st;
   if (!keep || !ws) return LETHE_ERR_INVALID;
+  if (layer_begin < 0 || layer_count < 0 || layer_begin > c->num_layers - layer_count) return LETHE_ERR_INVALID;
   if (ws_bytes < lethe_workspace_bytes(c, LETHE_OP_COMPACT)) return LETHE_ERR_WORKSPACE;
-  st = flush_pending(c, stream);
+  if (layer_count == 0) return LETHE_OK;
+  st = flush_pending(c, stream, layer_begin, layer_count);
   if (st != LETHE_OK) return st;
   CompactArgs a;
   a.k = c->k;
@@ -456,7 +462,8 @@ lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* w
   a.seq_base = c->seq_base;
   a.cap = c->cap;
   a.rows_per_layer = c->rows_per_layer;
-  a.L = c->num_layers;
+  a.l0 = layer_begin;
+  a.L = layer_count;
   a.B = c->num_seqs;
   a.HK = c->num_kv_heads;
   a.row_bytes = c->head_dim * (int32_t)elem_bytes(c->dtype);
@@ -477,6 +484,13 @@ lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* w
   a.hint = (int32_t*)((char*)c->state + sl.hint_off);
   a.dev_status = c->dev_status;
   return launch_compact(a, stream);
+}
+
+lethe_status lethe_kv_compact(const lethe_cache* c, const uint8_t* keep, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  lethe_status st = check_cache(c);
+  if (st != LETHE_OK) return st;
+  return lethe_kv_compact_layers(c, 0, c->num_layers, keep, ws, ws_bytes, stream);
 }
 
 lethe_status lethe_kv_compact_plan(const lethe_cache* c, const uint8_t* keep, void* plan, size_t plan_bytes,

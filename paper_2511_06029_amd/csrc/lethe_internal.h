@@ -189,7 +189,8 @@ struct FlushArgs {
   const int64_t* seq_base;
   const int32_t* cap;
   int64_t rows_per_layer;
-  int32_t L, B, HK;
+  int32_t l0;            // first layer of the launch
+  int32_t L, B, HK;      // L: layers of the launch (l0 .. l0 + L - 1)
   int32_t* pend_len;     // state, all layers
   const int32_t* pend_par;
   const float* pend_gamma;

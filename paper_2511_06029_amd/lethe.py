@@ -21,7 +21,7 @@ SHRINK_NO_BREAKPOINT, SHRINK_NOT_TRIGGERED = -1, -2
 EXPORTED = ("lethe_workspace_bytes", "lethe_state_bytes", "lethe_decode_attn_score", "lethe_decode_attn_score_final",
             "lethe_decode_attn_score_noalloc", "lethe_kv_compact_plan", "lethe_decode_attn_score_compact",
             "lethe_layer_sparsity", "lethe_rasr_select", "lethe_rasr_select_shared",
-            "lethe_segmented_shrink", "lethe_kv_compact", "lethe_score_flush",
+            "lethe_segmented_shrink", "lethe_kv_compact", "lethe_kv_compact_layers", "lethe_score_flush",
             "lethe_prefill_attn_score", "lethe_prefill_workspace_bytes", "lethe_status_string")
 
 
@@ -83,6 +83,8 @@ def load():
         lib.lethe_prefill_workspace_bytes.restype = sz
         lib.lethe_kv_compact.argtypes = [pc, vp, vp, sz, vp]
         lib.lethe_kv_compact.restype = ctypes.c_int
+        lib.lethe_kv_compact_layers.argtypes = [pc, i32, i32, vp, vp, sz, vp]
+        lib.lethe_kv_compact_layers.restype = ctypes.c_int
         lib.lethe_kv_compact_plan.argtypes = [pc, vp, vp, sz, vp]
         lib.lethe_kv_compact_plan.restype = ctypes.c_int
         lib.lethe_decode_attn_score_compact.argtypes = [pc, i32, vp, vp, vp, ctypes.c_float, ctypes.c_float, vp,
@@ -214,6 +216,14 @@ def kv_compact(cache, keep, ws, stream=None):
     st = load().lethe_kv_compact(ctypes.byref(cache.c_struct()), _p(keep), _p(ws),
                                  ws.numel() * ws.element_size(), _stream(stream))
     _check("lethe_kv_compact", st)
+
+
+def kv_compact_layers(cache, layer_begin, layer_count, keep, ws, stream=None):
+    """lethe_kv_compact_layers: the compaction of layers layer_begin ..
+    layer_begin + layer_count - 1 only."""
+    st = load().lethe_kv_compact_layers(ctypes.byref(cache.c_struct()), int(layer_begin), int(layer_count), _p(keep),
+                                        _p(ws), ws.numel() * ws.element_size(), _stream(stream))
+    _check("lethe_kv_compact_layers", st)
 
 
 def kv_compact_plan(cache, keep, plan, stream=None):
