@@ -51,6 +51,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kNumWaves = kThreads / kWave;
+constexpr long long kFlushBlocks = 2048;  // grid of a flush launch, at most
 constexpr float kNegBig = -1.0e30f;  // running-max start: finite, below any logit
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -1256,13 +1257,16 @@ __device__ void flush_segment_valu(const FlushArgs& a, int lb, int h, int l, int
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
-  const int lb = a.l0 * a.B + (int)blockIdx.x / a.HK;
-  const int h = (int)blockIdx.x % a.HK;
-  if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
-  const int P = a.pend_len[lb];
-  if (P <= 0) return;
-  flush_segment_valu<T, D, G>(a, lb, h, lb / a.B, lb % a.B, P);
-  flush_done(a, lb);
+  const long long nseg = (long long)a.L * a.B * a.HK;
+  for (long long i = blockIdx.x; i < nseg; i += gridDim.x) {
+    const int lb = a.l0 * a.B + (int)(i / a.HK);
+    const int h = (int)(i % a.HK);
+    if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
+    const int P = a.pend_len[lb];
+    if (P <= 0) continue;
+    flush_segment_valu<T, D, G>(a, lb, h, lb / a.B, lb % a.B, P);
+    flush_done(a, lb);
+  }
 }
 
 // bf16 flush on the matrix cores, the pending-update half of the decode
@@ -1350,13 +1354,16 @@ __device__ void flush_segment_bf16(const FlushArgs& a, int lb, int h, int l, int
 
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
-  const int lb = a.l0 * a.B + (int)blockIdx.x / a.HK;
-  const int h = (int)blockIdx.x % a.HK;
-  if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
-  const int P = a.pend_len[lb];
-  if (P <= 0) return;
-  flush_segment_bf16<D, G>(a, lb, h, lb / a.B, lb % a.B, P);
-  flush_done(a, lb);
+  const long long nseg = (long long)a.L * a.B * a.HK;
+  for (long long i = blockIdx.x; i < nseg; i += gridDim.x) {
+    const int lb = a.l0 * a.B + (int)(i / a.HK);
+    const int h = (int)(i % a.HK);
+    if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
+    const int P = a.pend_len[lb];
+    if (P <= 0) continue;
+    flush_segment_bf16<D, G>(a, lb, h, lb / a.B, lb % a.B, P);
+    flush_done(a, lb);
+  }
 }
 
 // Second launch of a settling call: s <- gamma s + sum_g exp2(x_g - M_g) / L_g
@@ -1505,10 +1512,13 @@ lethe_status launch_td(const DecodeArgs& a, int G, hipStream_t s) {
 
 template <typename T, int D, int G>
 lethe_status launch_flush_tdg(const FlushArgs& a, hipStream_t s) {
+  // Blocks walk the segments with a stride of the grid: with nothing pending
+  // (a settled step) the launch costs a few microseconds at any batch.
+  const unsigned nb = (unsigned)std::min<long long>((long long)a.L * a.B * a.HK, kFlushBlocks);
   if constexpr (sizeof(T) == 2)
-    hipLaunchKernelGGL((flush_bf16_kernel<D, G>), dim3((unsigned)(a.L * a.B * a.HK)), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((flush_bf16_kernel<D, G>), dim3(nb), dim3(kThreads), 0, s, a);
   else
-    hipLaunchKernelGGL((flush_kernel<T, D, G>), dim3((unsigned)(a.L * a.B * a.HK)), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((flush_kernel<T, D, G>), dim3(nb), dim3(kThreads), 0, s, a);
   return hipGetLastError() == hipSuccess ? LETHE_OK : LETHE_ERR_HIP;
 }
 
