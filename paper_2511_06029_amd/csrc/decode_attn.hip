@@ -1197,6 +1197,31 @@ constexpr auto decode_kernel() {
 // (layer, sequence, KV head); the last block of each (layer, sequence)
 // clears its pending length.
 // ---------------------------------------------------------------------------
+// The segments of a flush block: a contiguous run of at most kThreads.
+__device__ inline void flush_range(const FlushArgs& a, long long& i0, long long& n) {
+  const long long nseg = (long long)a.L * a.B * a.HK;
+  const long long per = (nseg + gridDim.x - 1) / gridDim.x;
+  i0 = (long long)blockIdx.x * per;
+  n = min(per, nseg - i0);
+  if (n < 0) n = 0;
+}
+
+// One load round for all of a block's segments: thread t reads segment
+// i0 + t's pending length into s_pend[t] and refreshes its (layer, sequence)'s
+// tiling hint.  Every segment belongs to one block, which reads its pending
+// length before it processes any segment, so the read always precedes the
+// clearing by the last block of that (layer, sequence).
+__device__ inline void flush_scan(const FlushArgs& a, long long i0, long long n, int* s_pend) {
+  const int t = threadIdx.x;
+  if (t < n) {
+    const long long i = i0 + t;
+    const int lb = a.l0 * a.B + (int)(i / a.HK);
+    if (i % a.HK == 0) a.hint[lb] = a.len[lb];
+    s_pend[t] = a.pend_len[lb];
+  }
+  __syncthreads();
+}
+
 // Every flush block of a (layer, sequence) with a pending step counts itself
 // once all its threads are done with the pending state; the last of the H_KV
 // blocks clears the pending length and the counter (which the decode state
@@ -1260,14 +1285,16 @@ __device__ void flush_segment_valu(const FlushArgs& a, int lb, int h, int l, int
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kThreads) void flush_kernel(FlushArgs a) {
-  const long long nseg = (long long)a.L * a.B * a.HK;
-  for (long long i = blockIdx.x; i < nseg; i += gridDim.x) {
-    const int lb = a.l0 * a.B + (int)(i / a.HK);
-    const int h = (int)(i % a.HK);
-    if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
-    const int P = a.pend_len[lb];
+  long long i0, n;
+  flush_range(a, i0, n);
+  __shared__ int s_pend[kThreads];
+  flush_scan(a, i0, n, s_pend);
+  for (int t = 0; t < n; ++t) {
+    const int P = s_pend[t];
     if (P <= 0) continue;
-    flush_segment_valu<T, D, G>(a, lb, h, lb / a.B, lb % a.B, P);
+    const long long i = i0 + t;
+    const int lb = a.l0 * a.B + (int)(i / a.HK);
+    flush_segment_valu<T, D, G>(a, lb, (int)(i % a.HK), lb / a.B, lb % a.B, P);
     flush_done(a, lb);
   }
 }
@@ -1357,14 +1384,16 @@ __device__ void flush_segment_bf16(const FlushArgs& a, int lb, int h, int l, int
 
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) void flush_bf16_kernel(FlushArgs a) {
-  const long long nseg = (long long)a.L * a.B * a.HK;
-  for (long long i = blockIdx.x; i < nseg; i += gridDim.x) {
-    const int lb = a.l0 * a.B + (int)(i / a.HK);
-    const int h = (int)(i % a.HK);
-    if (h == 0 && threadIdx.x == 0) a.hint[lb] = a.len[lb];
-    const int P = a.pend_len[lb];
+  long long i0, n;
+  flush_range(a, i0, n);
+  __shared__ int s_pend[kThreads];
+  flush_scan(a, i0, n, s_pend);
+  for (int t = 0; t < n; ++t) {
+    const int P = s_pend[t];
     if (P <= 0) continue;
-    flush_segment_bf16<D, G>(a, lb, h, lb / a.B, lb % a.B, P);
+    const long long i = i0 + t;
+    const int lb = a.l0 * a.B + (int)(i / a.HK);
+    flush_segment_bf16<D, G>(a, lb, (int)(i % a.HK), lb / a.B, lb % a.B, P);
     flush_done(a, lb);
   }
 }
@@ -1515,9 +1544,11 @@ lethe_status launch_td(const DecodeArgs& a, int G, hipStream_t s) {
 
 template <typename T, int D, int G>
 lethe_status launch_flush_tdg(const FlushArgs& a, hipStream_t s) {
-  // Blocks walk the segments with a stride of the grid: with nothing pending
-  // (a settled step) the launch costs a few microseconds at any batch.
-  const unsigned nb = (unsigned)std::min<long long>((long long)a.L * a.B * a.HK, kFlushBlocks);
+  // Each block takes a contiguous run of at most kThreads segments and reads
+  // their pending lengths in one round: with nothing pending (a settled
+  // step) the launch costs a few microseconds at any batch.
+  const long long nseg = (long long)a.L * a.B * a.HK;
+  const unsigned nb = (unsigned)std::min<long long>(nseg, std::max<long long>(kFlushBlocks, (nseg + kThreads - 1) / kThreads));
   if constexpr (sizeof(T) == 2)
     hipLaunchKernelGGL((flush_bf16_kernel<D, G>), dim3(nb), dim3(kThreads), 0, s, a);
   else
