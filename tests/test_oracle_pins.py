@@ -422,3 +422,77 @@ def test_prune_round_keeps_exactly_the_budgets():
         for l in range(L):
             for h in range(HK):
                 assert cache.K[l][b][h].shape[0] == budget[b, l]
+
+
+def _rank_keep(s32, k, recent, sink):
+    """Independent selection on fp32 scores: the protected windows (recent
+    first, then sinks, both within k), then the rest by numpy's lexsort on
+    (score descending with NaN last, row ascending)."""
+    n = len(s32)
+    keep = np.zeros(n, bool)
+    if k >= n:
+        keep[:] = True
+        return keep
+    k = max(k, 0)
+    r = min(recent, k)
+    sk = min(sink, k - r)
+    keep[n - r:] = True
+    keep[:sk] = True
+    cand = np.arange(sk, n - r)
+    v = s32[cand].astype(np.float64)
+    nan = np.isnan(v)
+    order = np.lexsort((cand, np.where(nan, 0.0, -v), nan))
+    keep[cand[order[:k - r - sk]]] = True
+    return keep
+
+
+@pytest.mark.parametrize("given_sparsity", [False, True])
+def test_prune_round_composition(given_sparsity):
+    """The whole round against its parts recomposed independently: each
+    (layer, sequence)'s sparsity from its own heads' summed scores (Hoyer in
+    numpy), the split fed those values in fp32, each head's kept set from its
+    own fp32 scores and its layer's budget, and K, V and scores compacted with
+    the same mask.  Segments carry distinct values, so a crossed layer,
+    sequence or head shows."""
+    L, B, HQ, HK, D = 4, 3, 6, 3, 16
+    rng = RNG(77)
+    cache = oracle.OracleCache(L, B, HQ, HK, D)
+    orig = {}
+    for l in range(L):
+        for b in range(B):
+            n = 60 + 37 * l + 11 * b
+            for h in range(HK):
+                K = rng.standard_normal((n, D)).astype(np.float32) + 100 * l + 10 * b + h
+                V = rng.standard_normal((n, D)).astype(np.float32) - 100 * l - 10 * b - h
+                s = synth.score_vector(rng, n, "zipf").astype(np.float64) * (1 + 0.3 * h + 0.1 * l)
+                s[rng.integers(0, n, 3)] = s[0]  # some ties
+                cache.set_segment(l, b, h, K, V, s)
+                orig[l, b, h] = (K.copy(), V.copy(), s.copy())
+    recent, sink = 8, 2
+    Gb = [L * 40, L * 55, L * 30]
+    s_in = None
+    if given_sparsity:
+        s_in = [[float(rng.random()) for _ in range(L)] for _ in range(B)]
+    S, budget, inf = cache.prune_round(Gb, recent, sink, sparsity_in=s_in)
+    for b in range(B):
+        S_ind = np.zeros(L)
+        for l in range(L):
+            if given_sparsity:
+                S_ind[l] = s_in[b][l]
+            else:
+                a = sum(orig[l, b, h][2] for h in range(HK))
+                n = len(a)
+                l1, l2 = np.abs(a).sum(), math.sqrt((a * a).sum())
+                S_ind[l] = min(max((math.sqrt(n) - l1 / l2) / (math.sqrt(n) - 1), 0.0), 1.0)
+        np.testing.assert_allclose(S[b], S_ind, rtol=1e-12, atol=1e-14)
+        n_l = np.array([len(orig[l, b, 0][2]) for l in range(L)], np.int32)
+        bud, infb = oracle.budget_split(n_l, S_ind.astype(np.float32), recent, sink, Gb[b])
+        np.testing.assert_array_equal(budget[b], bud)
+        assert inf[b] == infb
+        for l in range(L):
+            for h in range(HK):
+                K, V, s = orig[l, b, h]
+                keep = _rank_keep(s.astype(np.float32), int(budget[b, l]), recent, sink)
+                np.testing.assert_array_equal(cache.K[l][b][h], K[keep])
+                np.testing.assert_array_equal(cache.V[l][b][h], V[keep])
+                np.testing.assert_array_equal(cache.s[l][b][h], s[keep])
