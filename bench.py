@@ -383,7 +383,7 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
         last_kept = int(len_snap[windows].numpy().astype(np.int64).sum())
     status = int(cache.dev_status[0])
     if status != 0:
-        raise RuntimeError("device status bits set: %d" % status)
+        raise RuntimeError("device status bits set: %d (%s)" % (status, ", ".join(L.dev_status_names(status))))
     log("timed intervals done")
 
     # Work accounting from the length snapshots (lengths after each
@@ -590,7 +590,7 @@ def run_prefill(args):
     t1 = time.perf_counter()
     status = int(cache.dev_status[0])
     if status != 0:
-        raise RuntimeError("device status bits set: %d" % status)
+        raise RuntimeError("device status bits set: %d (%s)" % (status, ", ".join(L.dev_status_names(status))))
     elapsed = t1 - t0
     call_ms = float(np.sum([e[0].elapsed_time(e[1]) for e in ev])) / (args.steps * Lyr)
     # Algorithmic work of one call: causal Q K^T and P V once per query head,

@@ -100,6 +100,20 @@ def status_string(status):
     return load().lethe_status_string(int(status)).decode()
 
 
+DEV_STATUS_NAMES = ((DEV_APPEND_OVERFLOW, "append overflow"), (DEV_INFEASIBLE, "infeasible budget"),
+                    (DEV_BAD_LAYOUT, "bad layout"), (DEV_HEAD_MISMATCH, "head mismatch"),
+                    (DEV_WAIT_TIMEOUT, "wait timeout (results of that call unspecified)"))
+
+
+def dev_status_names(bits):
+    """The names of the device status bits set in `bits` (include/lethe.h)."""
+    names = [name for bit, name in DEV_STATUS_NAMES if int(bits) & bit]
+    rest = int(bits) & ~sum(bit for bit, _ in DEV_STATUS_NAMES)
+    if rest:
+        names.append("unknown bits %#x" % rest)
+    return names
+
+
 def _p(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 

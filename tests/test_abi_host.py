@@ -215,3 +215,20 @@ def test_struct_layout_matches_header():
     assert L.CCache.dev_status.offset == 80
     assert L.CCache.state.offset == 88
     assert ctypes.sizeof(L.CCache) == 96
+
+
+def test_device_status_bits_match_the_header():
+    """The binding's device status bits and their names against the
+    LETHE_DEV_* values include/lethe.h defines."""
+    import re
+    from paper_2511_06029_amd import lethe as Lb
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    text = open(os.path.join(root, "include", "lethe.h")).read()
+    defs = {m.group(1): int(m.group(2)) for m in re.finditer(r"#define LETHE_DEV_(\w+)\s+(\d+)", text)}
+    assert defs == {"APPEND_OVERFLOW": Lb.DEV_APPEND_OVERFLOW, "INFEASIBLE": Lb.DEV_INFEASIBLE,
+                    "BAD_LAYOUT": Lb.DEV_BAD_LAYOUT, "HEAD_MISMATCH": Lb.DEV_HEAD_MISMATCH,
+                    "WAIT_TIMEOUT": Lb.DEV_WAIT_TIMEOUT}
+    assert sorted(bit for bit, _ in Lb.DEV_STATUS_NAMES) == sorted(defs.values())
+    assert Lb.dev_status_names(0) == []
+    assert Lb.dev_status_names(Lb.DEV_WAIT_TIMEOUT | Lb.DEV_BAD_LAYOUT)[0] == "bad layout"
+    assert Lb.dev_status_names(1 << 12) == ["unknown bits 0x1000"]
