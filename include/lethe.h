@@ -160,7 +160,8 @@ size_t lethe_state_bytes(const lethe_cache* cache);
  * rows, one block each, so that sequences of very different lengths finish
  * together.  The split follows tiling hints, the layer's lengths as the
  * decode state last recorded them (lethe_score_flush, the prune calls, which
- * flush first, and lethe_kv_compact record them; a zero-filled state has
+ * flush first, lethe_kv_compact, lethe_kv_compact_layers and
+ * lethe_kv_compact_plan record them; a zero-filled state has
  * none, and the split is then the same for every segment).  The hints only
  * shape the split, never the result: a length changed since they were
  * recorded is still attended in full.  A segment's blocks take their 32-row

@@ -1,11 +1,12 @@
 // Decode attention fused with the RASR importance update (Eq. 5), gfx950.
 //
 // One launch handles one layer for every sequence.  Each (sequence, KV head)
-// segment gets nch blocks (split-K flash decoding), spread over the grid
-// (block i serves segment i mod segments).  The cached rows of a segment are
-// cut into 32-row steps that the segment's wavefronts take from a per-segment
-// counter, so a block that the memory system serves faster simply takes more
-// steps; no plan kernel and no length on the host.
+// segment gets chunks in proportion to its length (split-K flash decoding),
+// one block each; the lengths come from the layer's tiling hints in the
+// decode state, so every block derives the same map itself (no plan kernel,
+// no length on the host).  The cached rows of a segment are cut into 32-row
+// steps that the segment's wavefronts take from a per-segment counter, so a
+// block that the memory system serves faster simply takes more steps.
 //
 // Per wavefront and step (bf16 storage):
 //  - S^T = K Q^T on the matrix cores (v_mfma_f32_16x16x32_bf16: 16 rows x
@@ -29,10 +30,10 @@
 // leaves nothing pending; settle_kernel then applies its update with the same
 // arithmetic.
 //
-// Every block bumps its sequence's counter once it has read len and the
-// pending state; the block that finishes a segment publishes the new length
-// and pending step when the count is full (nobody of this launch reads them
-// afterwards).  With one block per segment the block writes out and the
+// Every block bumps its sequence's counter once all its wavefronts are past
+// their last use of len and the pending state; the block that finishes a
+// segment publishes the new length and pending step when the count is full
+// (nobody of this launch reads them afterwards).  With one block per segment the block writes out and the
 // step's (M, 1/L) itself.  Otherwise each block's (m, l, o) partial goes to
 // the workspace with write-through stores, then the block bumps its segment's
 // counter; the last block of a segment combines the partials.  Counters go
