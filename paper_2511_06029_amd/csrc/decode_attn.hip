@@ -921,6 +921,11 @@ __device__ inline int wave_incl_scan_i32(int v) {
 
 // Hinted steps are capped so that their sum over 1024 sequences stays an int.
 constexpr int kMaxHintSteps = 1 << 20;
+// Adaptive split: hinted steps per chunk it aims for, and the fewest chunks
+// (measured on the batch-128 ragged cache: its smallest layers do best near
+// 1024 chunks of about 11 steps, its largest near 4096 of about 45).
+constexpr long long kStepsPerChunk = 16;
+constexpr int kMinChunks = 1024;
 
 // The plan of block `blk` from R rows of 64 sequences (sequence 64 r + lane).
 // With kWords the sequences' own words come in the same round trip and the
@@ -957,7 +962,13 @@ __device__ inline BlockPlan plan_block(const DecodeArgs& a, int blk, SeqWords& w
   }
   const long long total = (long long)__builtin_amdgcn_readlane(wave_incl_scan_i32(sum), kWave - 1) * a.HK;
   int spb = 0;  // steps per chunk; 0: flat split
-  if (total > 0) spb = (int)min((total + a.nbt - 1) / a.nbt, (long long)kMaxHintSteps);
+  if (total > 0) {
+    // Chunks of about kStepsPerChunk hinted steps, between min(kMinChunks,
+    // nbt) and nbt chunks in all (nbt itself when the target is fixed).
+    long long nb = a.nbt;
+    if (a.adaptive) nb = min(max(total / kStepsPerChunk, (long long)min(kMinChunks, a.nbt)), (long long)a.nbt);
+    spb = (int)min((total + nb - 1) / nb, (long long)kMaxHintSteps);
+  }
   BlockPlan p;
   int carry = 0;
 #pragma unroll
@@ -1460,13 +1471,15 @@ int env_int(const char* name) {
   return v ? atoi(v) : 0;
 }
 
-// Chunks a launch aims for by default: one per 2048 rows of the layer's
-// capacity (the only size the host knows), between 512 and 2048.  Measured on
-// the model-scale workloads: the Llama-8B batch-8 and Qwen-7B batch-16 caches
-// (about 1M rows per layer, 0.3M live) do best with 512-1024 chunks, the
-// Llama-8B batch-128 cache (9M rows, 1.8M live) with 2048.
+// Chunks a launch may use by default: one per 2048 rows of the layer's
+// capacity (the only size the host knows), between 512 and 4096; the plan
+// then takes fewer for small hinted totals (kStepsPerChunk, kMinChunks).
+// Measured on the model-scale workloads: the Llama-8B batch-8 and Qwen-7B
+// batch-16 caches (about 1M rows per layer, 0.3M live) do best with 512-1024
+// chunks; the Llama-8B batch-128 cache (9M rows per layer, 0.35M-5.8M live by
+// layer) with about 1024 on its smallest layers and 4096 on its largest.
 constexpr int64_t kRowsPerTargetChunk = 2048;
-constexpr int64_t kMinTarget = 512, kMaxTarget = 2048;
+constexpr int64_t kMinTarget = 512, kMaxTarget = 4096;
 
 template <typename T, int D, int G, bool kCompact = false>
 lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
@@ -1479,6 +1492,7 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
     if (target > kMaxTarget) target = kMaxTarget;
   }
   a.deterministic = env_int("LETHE_DECODE_DETERMINISTIC") != 0;
+  a.adaptive = env_blocks <= 0;
   const int64_t segs = (int64_t)a.B * a.HK;
   // Flat split (no hints yet): at least four chunks per segment, so that with
   // many segments of ragged lengths the dispatcher hands the slots of early

@@ -125,7 +125,8 @@ struct DecodeArgs {
   float* part;           // workspace: one partial per block
   int64_t part_cap;      // chunk partials `part` holds (at least B * HK)
   int32_t* dev_status;
-  int32_t nbt;           // blocks the tiling aims for
+  int32_t nbt;           // blocks the tiling aims for (at most)
+  int32_t adaptive;      // fewer chunks for small hinted totals
   int32_t nch_flat;      // chunks per segment when every hint is 0
   int32_t deterministic; // fixed step schedule instead of the per-segment step counter
   // Compacting call only (else null): the plan lethe_kv_compact_plan wrote.
