@@ -172,9 +172,10 @@ size_t lethe_state_bytes(const lethe_cache* cache);
  * non-zero value every block's steps are fixed and repeated calls are
  * bit-identical (1.7% slower on the Llama-8B batch-128 workload, 4.4% on the
  * Qwen-7B batch-16 one).  By default a call splits its hinted rows into
- * chunks of about 16 steps, at least min(1024, N) and at most N chunks, N
- * being one per 2048 rows of capacity (512 to 4096); LETHE_DECODE_BLOCKS
- * fixes the number of chunks instead.
+ * chunks of about 14 steps, at least min(512, N) and at most N chunks, N
+ * being one per 1024 rows of capacity (512 to 4096); LETHE_DECODE_BLOCKS
+ * fixes the number of chunks instead, LETHE_DECODE_STEPS_PER_CHUNK and
+ * LETHE_DECODE_MIN_CHUNKS change the two defaults.
  * Accumulation is fp32; results match the exact result to about 1e-5
  * relative.  Errors: LETHE_ERR_INVALID (null pointer, layer out of range,
  * gamma outside (0, 1] or NaN, NaN scale), LETHE_ERR_UNSUPPORTED,

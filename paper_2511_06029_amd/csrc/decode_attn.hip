@@ -921,11 +921,6 @@ __device__ inline int wave_incl_scan_i32(int v) {
 
 // Hinted steps are capped so that their sum over 1024 sequences stays an int.
 constexpr int kMaxHintSteps = 1 << 20;
-// Adaptive split: hinted steps per chunk it aims for, and the fewest chunks
-// (measured on the batch-128 ragged cache: its smallest layers do best near
-// 1024 chunks of about 11 steps, its largest near 4096 of about 45).
-constexpr long long kStepsPerChunk = 16;
-constexpr int kMinChunks = 1024;
 
 // The plan of block `blk` from R rows of 64 sequences (sequence 64 r + lane).
 // With kWords the sequences' own words come in the same round trip and the
@@ -966,7 +961,7 @@ __device__ inline BlockPlan plan_block(const DecodeArgs& a, int blk, SeqWords& w
     // Chunks of about kStepsPerChunk hinted steps, between min(kMinChunks,
     // nbt) and nbt chunks in all (nbt itself when the target is fixed).
     long long nb = a.nbt;
-    if (a.adaptive) nb = min(max(total / kStepsPerChunk, (long long)min(kMinChunks, a.nbt)), (long long)a.nbt);
+    if (a.adaptive) nb = min(max(total / a.steps_per_chunk, (long long)min(a.min_chunks, a.nbt)), (long long)a.nbt);
     spb = (int)min((total + nb - 1) / nb, (long long)kMaxHintSteps);
   }
   BlockPlan p;
@@ -1471,15 +1466,20 @@ int env_int(const char* name) {
   return v ? atoi(v) : 0;
 }
 
-// Chunks a launch may use by default: one per 2048 rows of the layer's
+// Chunks a launch may use by default: one per 1024 rows of the layer's
 // capacity (the only size the host knows), between 512 and 4096; the plan
-// then takes fewer for small hinted totals (kStepsPerChunk, kMinChunks).
-// Measured on the model-scale workloads: the Llama-8B batch-8 and Qwen-7B
-// batch-16 caches (about 1M rows per layer, 0.3M live) do best with 512-1024
-// chunks; the Llama-8B batch-128 cache (9M rows per layer, 0.35M-5.8M live by
-// layer) with about 1024 on its smallest layers and 4096 on its largest.
-constexpr int64_t kRowsPerTargetChunk = 2048;
+// takes about kStepsPerChunk hinted steps a chunk within that, and at least
+// kMinChunks.  Measured with per-dispatch traces: the Qwen-7B batch-16 cache
+// (64 segments of about 5k rows) does best near 768 chunks (14 steps), the
+// Llama-8B batch-8 one near 512 (16 steps); the Llama-8B batch-128 ragged
+// cache (1024 segments, 0.35M-5.8M live rows by layer) near 800-1024 on its
+// smallest layers and 4096 on its largest.
+constexpr int64_t kRowsPerTargetChunk = 1024;
 constexpr int64_t kMinTarget = 512, kMaxTarget = 4096;
+// Adaptive split: hinted steps per chunk a call aims for, and the fewest
+// chunks (LETHE_DECODE_STEPS_PER_CHUNK, LETHE_DECODE_MIN_CHUNKS override).
+constexpr int kStepsPerChunk = 14;
+constexpr int kMinChunks = 512;
 
 template <typename T, int D, int G, bool kCompact = false>
 lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
@@ -1493,6 +1493,10 @@ lethe_status launch_tdg(const DecodeArgs& a_in, hipStream_t s) {
   }
   a.deterministic = env_int("LETHE_DECODE_DETERMINISTIC") != 0;
   a.adaptive = env_blocks <= 0;
+  const int env_spc = env_int("LETHE_DECODE_STEPS_PER_CHUNK");
+  const int env_minc = env_int("LETHE_DECODE_MIN_CHUNKS");
+  a.steps_per_chunk = env_spc > 0 ? env_spc : kStepsPerChunk;
+  a.min_chunks = env_minc > 0 ? env_minc : kMinChunks;
   const int64_t segs = (int64_t)a.B * a.HK;
   // Flat split (no hints yet): at least four chunks per segment, so that with
   // many segments of ragged lengths the dispatcher hands the slots of early

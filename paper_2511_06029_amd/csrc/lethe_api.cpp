@@ -184,6 +184,8 @@ DecodeArgs decode_args(const lethe_cache* c, int32_t layer, const void* q, const
   a.dev_status = c->dev_status;
   a.nbt = a.nch_flat = 0;  // chosen by the launcher
   a.adaptive = 0;
+  a.steps_per_chunk = 16;
+  a.min_chunks = 1024;
   a.deterministic = 0;
   a.logit = settle ? (float*)((char*)ws + decode_final_logit_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
   a.apply_rows = settle ? (int32_t*)((char*)ws + decode_final_rows_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;

@@ -127,6 +127,8 @@ struct DecodeArgs {
   int32_t* dev_status;
   int32_t nbt;           // blocks the tiling aims for (at most)
   int32_t adaptive;      // fewer chunks for small hinted totals
+  int32_t steps_per_chunk; // adaptive split: hinted steps a chunk aims for
+  int32_t min_chunks;    // adaptive split: fewest chunks (at most nbt)
   int32_t nch_flat;      // chunks per segment when every hint is 0
   int32_t deterministic; // fixed step schedule instead of the per-segment step counter
   // Compacting call only (else null): the plan lethe_kv_compact_plan wrote.
