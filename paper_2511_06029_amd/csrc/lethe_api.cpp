@@ -183,9 +183,7 @@ DecodeArgs decode_args(const lethe_cache* c, int32_t layer, const void* q, const
   a.part_cap = (int64_t)(part_bytes / ((size_t)part_stride(G, D) * sizeof(float)));
   a.dev_status = c->dev_status;
   a.nbt = a.nch_flat = 0;  // chosen by the launcher
-  a.adaptive = 0;
-  a.steps_per_chunk = 16;
-  a.min_chunks = 1024;
+  a.adaptive = a.steps_per_chunk = a.min_chunks = 0;  // chosen by the launcher
   a.deterministic = 0;
   a.logit = settle ? (float*)((char*)ws + decode_final_logit_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
   a.apply_rows = settle ? (int32_t*)((char*)ws + decode_final_rows_off(c->num_seqs, c->num_kv_heads, G, D)) : nullptr;
