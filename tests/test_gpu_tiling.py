@@ -4,8 +4,9 @@ record in the decode state).
 
 Checked against the oracle (|gpu - ref| <= 1e-3 + 2e-3 |ref|): the flat
 split (no hints yet), the hinted split, hints that no longer match the
-lengths (the split then only balances worse), several block targets and the
-fixed step schedule.  With the fixed schedule repeated calls on twin caches
+lengths (the split then only balances worse), several block targets, the
+adaptive chunk count at its extremes (one step a chunk, the fewest chunks,
+always the most) and the fixed step schedule.  With the fixed schedule repeated calls on twin caches
 are bit-identical.
 """
 import math
@@ -55,8 +56,12 @@ def step(H, rng, gamma=0.95):
 
 @pytest.mark.parametrize("env", [{}, {"LETHE_DECODE_BLOCKS": "1"}, {"LETHE_DECODE_BLOCKS": "3"},
                                  {"LETHE_DECODE_BLOCKS": "8192"}, {"LETHE_DECODE_DETERMINISTIC": "1"},
-                                 {"LETHE_DECODE_DETERMINISTIC": "1", "LETHE_DECODE_BLOCKS": "3"}],
-                         ids=["default", "blocks1", "blocks3", "blocks8192", "fixed", "fixed-blocks3"])
+                                 {"LETHE_DECODE_DETERMINISTIC": "1", "LETHE_DECODE_BLOCKS": "3"},
+                                 {"LETHE_DECODE_STEPS_PER_CHUNK": "1"},
+                                 {"LETHE_DECODE_STEPS_PER_CHUNK": "100000", "LETHE_DECODE_MIN_CHUNKS": "1"},
+                                 {"LETHE_DECODE_MIN_CHUNKS": "100000"}],
+                         ids=["default", "blocks1", "blocks3", "blocks8192", "fixed", "fixed-blocks3",
+                              "adaptive-1step", "adaptive-fewest", "adaptive-all"])
 def test_tiling_flat_hinted_and_stale(env, monkeypatch):
     for k, v in env.items():
         monkeypatch.setenv(k, v)
