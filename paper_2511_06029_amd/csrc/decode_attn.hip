@@ -887,9 +887,10 @@ struct AttnLds<float, D> {
 // 32-row steps, so that sequences of very different lengths end together.
 // The split follows the layer's tiling hints (lengths in the decode state,
 // written by flush and compaction only, so every block of a launch reads the
-// same values): with S the hinted steps of all segments and nbt the blocks
-// the launch aims for, a segment of w hinted steps gets
-// nch = clamp(ceil(w / ceil(S / nbt)), 1, kMaxChunksPerSeg) chunks, one
+// same values): with S the hinted steps of all segments and nb the chunks
+// the call aims for (S / steps_per_chunk between min(min_chunks, nbt) and
+// nbt, or nbt itself when the target is fixed), a segment of w hinted steps
+// gets nch = clamp(ceil(w / ceil(S / nb)), 1, kMaxChunksPerSeg) chunks, one
 // block each.  The blocks of sequence b are consecutive, KV head by KV head:
 // block P_b + h nch_b + c is chunk c of segment (b, h).  When every hint is 0
 // each segment gets nch_flat chunks.  A hint only shapes the split: every
@@ -958,8 +959,9 @@ __device__ inline BlockPlan plan_block(const DecodeArgs& a, int blk, SeqWords& w
   const long long total = (long long)__builtin_amdgcn_readlane(wave_incl_scan_i32(sum), kWave - 1) * a.HK;
   int spb = 0;  // steps per chunk; 0: flat split
   if (total > 0) {
-    // Chunks of about kStepsPerChunk hinted steps, between min(kMinChunks,
-    // nbt) and nbt chunks in all (nbt itself when the target is fixed).
+    // Chunks of about steps_per_chunk hinted steps, between
+    // min(min_chunks, nbt) and nbt chunks in all (nbt when the target is
+    // fixed).
     long long nb = a.nbt;
     if (a.adaptive) nb = min(max(total / a.steps_per_chunk, (long long)min(a.min_chunks, a.nbt)), (long long)a.nbt);
     spb = (int)min((total + nb - 1) / nb, (long long)kMaxHintSteps);
