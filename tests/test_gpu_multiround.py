@@ -8,15 +8,19 @@ selection, Section 4.2; compaction), and decoding again on the compacted
 cache with the tiling hints the compaction rewrote.  Three rounds, each
 compaction carried out one of three ways: whole cache in the round, layer by
 layer on a second stream with each layer's next decode step waiting for its
-own layer, or by the next decode step itself.
+own layer, or by the next decode step itself.  The kept sets come from RASR
+per KV head, RASR on the head-summed score (one set per layer and sequence),
+or Algorithm 1 with its size trigger, whose eviction thresholds carry over
+from round to round on the device.
 
 The oracle follows every step; after a round it drops the rows the device's
 keep mask drops, from its own K, V and score arrays, so that it goes on
 independently of the device's arithmetic.  Checked every step: outputs within
 1e-3 + 2e-3 |ref|.  Every interval's end: lengths and K, V rows bit for bit,
 scores within the output tolerance.  Every round: sparsities against the
-oracle's on the device's scores (1e-6) and on its own (1e-4), budgets and keep
-masks bit-exact given the device's sparsities and scores.
+oracle's on the device's scores (1e-6) and on its own (1e-4), budgets, keep
+masks, breakpoints and thresholds bit-exact given the device's sparsities and
+scores.
 """
 import math
 import sys
@@ -36,6 +40,7 @@ LAYERS, G, HK, D = 3, 4, 2, 128
 LENGTHS = [700, 2500, 0, 33, 1300]
 STEPS, ROUNDS = 8, 3          # steps per interval, prune rounds
 RECENT, SINK, KEEP_FRAC = 16, 2, 0.6
+SEGMENTS, TAU = 8, 3.0        # Algorithm 1's cut points and ratio
 
 
 def note(msg):
@@ -105,42 +110,63 @@ def interval(H, rng, ctx, r):
                 close(host(c.score[l, s:s + n]), H.orc.s[l][b][h], "scores round %d l%d b%d h%d" % (r, l, b, h))
 
 
-def prune(H, ctx, mode, r):
+def prune(H, ctx, mode, rule, r):
     c, B = H.c, H.c.B
     lens = host(c.len).astype(np.int64)
-    gb_host = np.zeros(B, np.int64)
-    for b in range(B):
-        protected = sum(min(int(lens[l, b]), RECENT + SINK) for l in range(LAYERS))
-        gb_host[b] = max(int(KEEP_FRAC * lens[:, b].sum()), protected)
-    gb = torch.from_numpy(gb_host).to(DEV)
-    S = torch.empty((B, LAYERS), dtype=torch.float32, device=DEV)
-    bud = torch.empty((B, LAYERS), dtype=torch.int32, device=DEV)
-    L.layer_sparsity(c, gb, RECENT, SINK, None, S, bud)
     keep = torch.full((LAYERS, c.rows_per_layer), 7, dtype=torch.uint8, device=DEV)
-    L.rasr_select(c, bud, RECENT, SINK, keep)
+    if rule == "shrink":
+        thr = host(ctx["evict"]).copy()
+        bp = torch.full((LAYERS, B), 99, dtype=torch.int32, device=DEV)
+        L.segmented_shrink(c, SEGMENTS, TAU, RECENT, SINK, ctx["evict"], bp, keep)
+    else:
+        gb_host = np.zeros(B, np.int64)
+        for b in range(B):
+            protected = sum(min(int(lens[l, b]), RECENT + SINK) for l in range(LAYERS))
+            gb_host[b] = max(int(KEEP_FRAC * lens[:, b].sum()), protected)
+        gb = torch.from_numpy(gb_host).to(DEV)
+        S = torch.empty((B, LAYERS), dtype=torch.float32, device=DEV)
+        bud = torch.empty((B, LAYERS), dtype=torch.int32, device=DEV)
+        L.layer_sparsity(c, gb, RECENT, SINK, None, S, bud)
+        (L.rasr_select_shared if rule == "shared" else L.rasr_select)(c, bud, RECENT, SINK, keep)
     torch.cuda.synchronize()
-    Sh, bh, kh = host(S), host(bud), host(keep)
+    kh = host(keep)
     score = host(c.score)
     masks = {}
     for b in range(B):
-        S_dev_scores = np.zeros(LAYERS)
+        heads = {}
         for l in range(LAYERS):
             n = int(lens[l, b])
-            heads = np.stack([score[l, s:s + n] for s, _ in (c.seg_rows(b, h) for h in range(HK))])
-            S_dev_scores[l] = oracle.layer_sparsity(heads)
-            assert abs(Sh[b, l] - S_dev_scores[l]) <= 1e-6, (r, b, l, Sh[b, l], S_dev_scores[l])
-            assert abs(Sh[b, l] - H.orc.sparsity(l, b)) <= 1e-4, (r, b, l, Sh[b, l], H.orc.sparsity(l, b))
-        want, infeasible = oracle.budget_split(lens[:, b].astype(np.int32), Sh[b], RECENT, SINK, gb_host[b])
-        assert not infeasible
-        np.testing.assert_array_equal(bh[b], want, err_msg="budgets round %d b%d" % (r, b))
+            heads[l] = np.stack([score[l, s:s + n] for s, _ in (c.seg_rows(b, h) for h in range(HK))])
+        if rule == "shrink":
+            evh, bph = host(ctx["evict"]), host(bp)
+            for l in range(LAYERS):
+                want, wbp, wlev = oracle.segmented_shrink(oracle.head_sum_f32(heads[l]), SEGMENTS, TAU, RECENT, SINK,
+                                                          thr[l, b])
+                assert (int(bph[l, b]), int(evh[l, b])) == (wbp, wlev), (r, l, b, thr[l, b])
+                ctx["cuts"] += wbp >= 0
+                for h in range(HK):
+                    masks[l, b, h] = want
+        else:
+            Sh, bh = host(S), host(bud)
+            for l in range(LAYERS):
+                S_dev_scores = oracle.layer_sparsity(heads[l])
+                assert abs(Sh[b, l] - S_dev_scores) <= 1e-6, (r, b, l, Sh[b, l], S_dev_scores)
+                assert abs(Sh[b, l] - H.orc.sparsity(l, b)) <= 1e-4, (r, b, l, Sh[b, l], H.orc.sparsity(l, b))
+            want, infeasible = oracle.budget_split(lens[:, b].astype(np.int32), Sh[b], RECENT, SINK, gb_host[b])
+            assert not infeasible
+            np.testing.assert_array_equal(bh[b], want, err_msg="budgets round %d b%d" % (r, b))
+            for l in range(LAYERS):
+                for h in range(HK):
+                    if rule == "shared":
+                        masks[l, b, h] = oracle.rasr_select_shared(heads[l], int(bh[b, l]), RECENT, SINK)
+                    else:
+                        masks[l, b, h] = oracle.rasr_select(heads[l][h], int(bh[b, l]), RECENT, SINK)
         for l in range(LAYERS):
             n = int(lens[l, b])
             for h in range(HK):
                 s, _ = c.seg_rows(b, h)
-                m = oracle.rasr_select(score[l, s:s + n], int(bh[b, l]), RECENT, SINK)
-                np.testing.assert_array_equal(kh[l, s:s + n], m.astype(np.uint8),
+                np.testing.assert_array_equal(kh[l, s:s + n], masks[l, b, h].astype(np.uint8),
                                               err_msg="keep round %d l%d b%d h%d" % (r, l, b, h))
-                masks[l, b, h] = m
     note("round %d: %d of %d rows kept" % (r, sum(int(m.sum()) for m in masks.values()), int(lens.sum()) * HK))
     if mode == "eager":
         L.kv_compact(c, keep, ctx["ws_c"])
@@ -166,22 +192,30 @@ def prune(H, ctx, mode, r):
         H.orc.s[l][b][h] = oracle.compact(H.orc.s[l][b][h], m)
 
 
+@pytest.mark.parametrize("rule", ["rasr", "shared", "shrink"])
 @pytest.mark.parametrize("mode", ["eager", "layers", "fused"])
-def test_decode_prune_rounds(mode):
-    note("multi-round %s" % mode)
-    rng = np.random.default_rng({"eager": 31, "layers": 32, "fused": 33}[mode])
+def test_decode_prune_rounds(mode, rule):
+    note("multi-round %s %s" % (mode, rule))
+    rng = np.random.default_rng(31 + 3 * ["eager", "layers", "fused"].index(mode) + ["rasr", "shared", "shrink"].index(rule))
     H = make(rng)
     c = H.c
+    # Size-trigger thresholds: pruning from the first round on, once past
+    # 1000 tokens, and never (above any length here).
+    thr = np.tile(np.array([0, 1000, 1 << 20, 0, 1000], np.int32), (LAYERS, 1))
     ctx = {"ws_final": c.workspace(L.OP_DECODE_FINAL), "plan": None, "done": None,
            "ws_c": c.workspace(L.OP_COMPACT_PLAN if mode == "fused" else L.OP_COMPACT),
-           "side": torch.cuda.Stream(device=DEV) if mode == "layers" else None}
+           "side": torch.cuda.Stream(device=DEV) if mode == "layers" else None,
+           "evict": torch.from_numpy(thr).to(DEV), "cuts": 0}
     for r in range(ROUNDS):
         interval(H, rng, ctx, r)
-        prune(H, ctx, mode, r)
+        prune(H, ctx, mode, rule, r)
     interval(H, rng, ctx, ROUNDS)
     assert int(c.dev_status[0]) == 0, L.dev_status_names(int(c.dev_status[0]))
-    # Every sequence was pruned below what it would hold unpruned.
-    lens = host(c.len)
-    for b, n in enumerate(LENGTHS):
-        if n > 100:
-            assert (lens[:, b] < n + STEPS * (ROUNDS + 1)).all(), (b, lens[:, b])
+    if rule == "shrink":
+        assert ctx["cuts"] > 0          # some rounds found a breakpoint
+    else:
+        # The long sequences were pruned below what they would hold unpruned.
+        lens = host(c.len)
+        for b, n in enumerate(LENGTHS):
+            if n > 100:
+                assert (lens[:, b] < n + STEPS * (ROUNDS + 1)).all(), (b, lens[:, b])
