@@ -427,36 +427,10 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
     select_gbs = sel_rows * HK * 5 / (float(np.sum(select_ms)) / 1e3) / 1e9
 
     value = tokens / elapsed
-    # What each prune round costs against the decode time it saves over the
-    # next interval: per-step decode time is fit as a + b * (cached tokens)
-    # over every interval of the run (warm-up included), and round w saves
-    # interval * b * (tokens it evicted).
     all_dec = np.array([ms(w, 1, 3) for w in range(windows)]) / (interval - 1)
     all_prune = np.array([ms(w, 3, 6) + extra[w] for w in range(windows)])
-    start_rows = np.array([int(kept0[w].sum()) for w in range(windows)] +
-                          [int(len_snap[windows].numpy().astype(np.int64).sum())])
-    mid_rows = start_rows[:windows] + Lyr * B * (interval + 2) / 2.0
-    prune_vs_saved = None
-    # The fit needs intervals of clearly different sizes (a run that starts
-    # at the steady state has none).
-    if windows >= 2 and np.ptp(mid_rows) >= 0.1 * mid_rows.mean():
-        slope, icpt = np.polyfit(mid_rows, all_dec, 1)
-        ratios = []
-        for w in range(windows):
-            # Rows the round after interval w dropped: the rows at its end less
-            # the rows the next interval starts from.
-            end_rows = start_rows[w] + Lyr * B * interval
-            nxt = start_rows[w + 1] if w + 1 < windows else last_kept
-            evicted = end_rows - nxt
-            saved_ms = interval * slope * evicted
-            ratios.append(float(all_prune[w] / saved_ms) if saved_ms > 0 else None)
-        steady = [r for r in ratios[1:] if r is not None]
-        prune_vs_saved = {
-            "round1": ratios[0], "steady_median": float(np.median(steady)) if steady else None,
-            "per_round": ratios, "decode_ms_per_token_step": float(slope), "decode_step_fixed_ms": float(icpt),
-            "prune_round_ms": [float(x) for x in all_prune],
-            "fused_step_extra_ms": [float(x) for x in extra],
-        }
+    start_rows = np.array([int(kept0[w].sum()) for w in range(windows)])
+    prune_vs_saved = prune_against_saved(all_dec, all_prune, start_rows, last_kept, Lyr * B, interval, extra)
     workload = WORKLOADS[cfg_id]
     if policy_name == "lethe-shared":
         workload += ", one kept set per layer and sequence"
@@ -514,6 +488,41 @@ def run_decode(args, cfg_id, steps, warmup, interval, policy_name, log, copy_pro
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def prune_against_saved(dec_step_ms, prune_ms, start_rows, last_kept, rows_per_step, interval, extra_ms):
+    """What each prune round costs against the decode time it saves over the
+    next interval.  dec_step_ms[w]: average decode step of interval w (ms);
+    prune_ms[w]: the round after it; start_rows[w]: cached rows (all layers,
+    sequences) when interval w starts; last_kept: rows after the last round;
+    rows_per_step: rows one decode step appends (layers x sequences).
+
+    The per-step decode time is fit as a + b * (cached rows at the interval's
+    middle) over every interval, and the round after interval w saves
+    interval * b * (rows it evicted): the rows at the interval's end less the
+    rows the next interval starts from.  Returns None when the intervals do
+    not differ enough in size for the fit (a run that starts at the steady
+    state)."""
+    import numpy as np
+    windows = len(dec_step_ms)
+    start_rows = np.asarray(start_rows, np.float64)
+    mid_rows = start_rows + rows_per_step * (interval + 2) / 2.0
+    if windows < 2 or np.ptp(mid_rows) < 0.1 * mid_rows.mean():
+        return None
+    slope, icpt = np.polyfit(mid_rows, np.asarray(dec_step_ms, np.float64), 1)
+    ratios = []
+    for w in range(windows):
+        end_rows = start_rows[w] + rows_per_step * interval
+        nxt = start_rows[w + 1] if w + 1 < windows else last_kept
+        saved_ms = interval * slope * (end_rows - nxt)
+        ratios.append(float(prune_ms[w] / saved_ms) if saved_ms > 0 else None)
+    steady = [r for r in ratios[1:] if r is not None]
+    return {
+        "round1": ratios[0], "steady_median": float(np.median(steady)) if steady else None,
+        "per_round": ratios, "decode_ms_per_token_step": float(slope), "decode_step_fixed_ms": float(icpt),
+        "prune_round_ms": [float(x) for x in prune_ms],
+        "fused_step_extra_ms": [float(x) for x in extra_ms],
+    }
 
 
 def run_prefill(args):
