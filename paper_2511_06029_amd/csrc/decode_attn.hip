@@ -367,12 +367,17 @@ __device__ void attn_chunk_mfma(const DecodeArgs& a, const Chunk& ck, const Read
       }
     }
   };
+  // V lines are read whole, once per call, so their loads carry the
+  // non-temporal policy (the `nt` bit): they leave L2 early, and the K lines
+  // (whose two 64-byte halves come from two loads) and the call's small
+  // shared data stay.  K loads keep the default policy.
+  constexpr int kVLoadPolicy = 2;  // nt
   auto load_v = [&](int bs) {
 #pragma unroll
     for (int u = 0; u < VLOADS; ++u) {
       const int row = min(bs + u + VLOADS * (lane / LPR), re - 1);
       __builtin_amdgcn_global_load_lds((global_cvoid_t*)(Vb + (long long)row * ROWB + 16 * (lane % LPR)),
-                                       (lds_void_t*)((lds_char_t*)vb + u * Cfg::VBLK), 16, 0, 0);
+                                       (lds_void_t*)((lds_char_t*)vb + u * Cfg::VBLK), 16, 0, kVLoadPolicy);
     }
   };
   int fixed_next = ck.first + w + ck.stride;
