@@ -1014,11 +1014,13 @@ __device__ inline void decode_body(const DecodeArgs& a) {
 
   // Every wave plans alike (no barrier); with up to 256 sequences the chosen
   // sequence's words arrive with the hints (one round of 64 sequences up to
-  // 64, four up to 256).
+  // 64, two up to 128, four up to 256).
   SeqWords sw;
   BlockPlan bp;
   if (a.B <= kWave) {
     bp = plan_block<1, true>(a, blk, sw);
+  } else if (a.B <= 2 * kWave) {
+    bp = plan_block<2, true>(a, blk, sw);
   } else if (a.B <= 4 * kWave) {
     bp = plan_block<4, true>(a, blk, sw);
   } else {
