@@ -170,8 +170,8 @@ size_t lethe_state_bytes(const lethe_cache* cache);
  * repeated calls on identical inputs can differ in the last bits of out and
  * score.  With the environment variable LETHE_DECODE_DETERMINISTIC set to a
  * non-zero value every block's steps are fixed and repeated calls are
- * bit-identical (1.7% slower on the Llama-8B batch-128 workload, 4.4% on the
- * Qwen-7B batch-16 one).  By default a call splits its hinted rows into
+ * bit-identical (about 3% slower on the Llama-8B batch-128 workload, 5% on
+ * the Qwen-7B batch-16 one).  By default a call splits its hinted rows into
  * chunks of about 14 steps, at least min(512, N) and at most N chunks, N
  * being one per 1024 rows of capacity (512 to 4096); LETHE_DECODE_BLOCKS
  * fixes the number of chunks instead, LETHE_DECODE_STEPS_PER_CHUNK and
