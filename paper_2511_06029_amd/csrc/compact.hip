@@ -335,7 +335,9 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
     }
     __syncthreads();
     // Rows whose destination is their source (before the first evicted row
-    // of the segment's first moved tile) are left alone.
+    // of the segment's first moved tile) are left alone.  K and V rows are
+    // copied once and not touched again in this launch: their loads and
+    // stores carry the non-temporal policy.
     u32x4_t rk[PASSES], rv[PASSES];
     float rs[PASSES];
     unsigned moved = 0;  // bit p: the row of pass p moves
@@ -346,8 +348,8 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
         const int src = s_src[i];
         if (src != it.base + i) {
           moved |= 1u << p;
-          rk[p] = *reinterpret_cast<const u32x4_t*>(K + (long long)src * RB + sub * 16);
-          rv[p] = *reinterpret_cast<const u32x4_t*>(V + (long long)src * RB + sub * 16);
+          rk[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(K + (long long)src * RB + sub * 16));
+          rv[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(V + (long long)src * RB + sub * 16));
           rs[p] = sub == 0 ? S[src] : 0.0f;
         }
       }
@@ -387,8 +389,8 @@ __global__ __launch_bounds__(kThreads) void compact_move_kernel(CompactArgs a) {
       const long long dst = it.base + i;
       // (Not s_src: threads already on the next tile may be rewriting it.)
       if ((moved >> p) & 1u) {
-        *reinterpret_cast<u32x4_t*>(K + dst * RB + sub * 16) = rk[p];
-        *reinterpret_cast<u32x4_t*>(V + dst * RB + sub * 16) = rv[p];
+        __builtin_nontemporal_store(rk[p], reinterpret_cast<u32x4_t*>(K + dst * RB + sub * 16));
+        __builtin_nontemporal_store(rv[p], reinterpret_cast<u32x4_t*>(V + dst * RB + sub * 16));
         if (sub == 0) S[dst] = rs[p];
       }
     }
