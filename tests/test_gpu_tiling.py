@@ -122,13 +122,17 @@ def test_fixed_schedule_is_bit_reproducible(monkeypatch):
     assert_same(live_scores(A), live_scores(Tw), "scores")
 
 
-def test_many_sequences_plan_path():
-    """More than 256 sequences (the plan reads the hints in 16 rows and the
-    chosen sequence's words afterwards), lengths log-uniform 1 .. 3000."""
-    rng = np.random.default_rng(13)
-    lengths = [int(x) for x in np.exp(rng.uniform(0, math.log(3000), size=300))]
+@pytest.mark.parametrize("nseq", [65, 128, 129, 256, 300])
+def test_sequence_counts_plan_paths(nseq):
+    """The block plan reads the hints of 64 sequences a round: with the chosen
+    sequence's words in the same round up to 256 sequences (two rounds up to
+    128, four up to 256), and in 16 rounds and a second load above that.
+    Lengths log-uniform 1 .. 3000, one of them empty; the first step splits
+    flat, the later ones by the hints the flush records."""
+    rng = np.random.default_rng(13 + nseq)
+    lengths = [int(x) for x in np.exp(rng.uniform(0, math.log(3000), size=nseq))]
     lengths[5] = 0
-    note("tiling: 300 sequences")
+    note("tiling: %d sequences" % nseq)
     HK, G, D = 1, 4, 64
     H = Harness(1, [n + 4 for n in lengths], G * HK, HK, D, "bf16")
     for b, n in enumerate(lengths):
@@ -142,6 +146,6 @@ def test_many_sequences_plan_path():
         kn = rng.standard_normal((len(lengths), HK, D))
         vn = rng.standard_normal((len(lengths), HK, D))
         out, ref = H.decode(0, q.astype(np.float32), kn.astype(np.float32), vn.astype(np.float32), 0.9, 0.0)
-        close(out, ref, "300 sequences, step %d" % t)
+        close(out, ref, "%d sequences, step %d" % (nseq, t))
     H.check_scores(0)
     assert int(H.c.dev_status[0]) == 0
